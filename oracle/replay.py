@@ -1,0 +1,110 @@
+"""Metadata-only policy passes and state reconstruction (oracle; test infrastructure only).
+
+Eviction depends only on row metadata (segment class, unit id) and the
+resident count, never on K/V values (Sec. 3.3 counts positions), so a whole
+stream's eviction history can be replayed without attention.  The resident
+state after any step is then fully determined, which lets a test resume a
+long stream at unit k by regenerating only the surviving rows' values.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+from synth.streams import StreamSpec, WorkloadConfig, step_values
+
+from .cache import OracleCache
+from .policy import plan_eviction
+
+
+@dataclass
+class StepTrace:
+    n_pre: int
+    n_post: int
+    units: List[int]
+    budget_unmet: bool
+    moved: int                 # survivors at or after the first evicted slot
+
+
+@dataclass
+class StreamTrace:
+    steps: List[StepTrace] = field(default_factory=list)
+    peak: int = 0
+    # layout after the last replayed step, and where each row came from
+    pos: Optional[np.ndarray] = None
+    seg: Optional[np.ndarray] = None
+    unit: Optional[np.ndarray] = None
+    src_step: Optional[np.ndarray] = None
+    src_row: Optional[np.ndarray] = None
+
+
+def replay_metadata(spec: StreamSpec, budget: int, window: int,
+                    n_steps: Optional[int] = None, evict: bool = True) -> StreamTrace:
+    """Run the eviction policy over the first ``n_steps`` steps of a stream."""
+    n_steps = len(spec.steps) if n_steps is None else n_steps
+    pos = np.zeros(0, np.int64)
+    seg = np.zeros(0, np.uint8)
+    unit = np.zeros(0, np.int64)
+    src_step = np.zeros(0, np.int64)
+    src_row = np.zeros(0, np.int64)
+    cur = -1
+    tr = StreamTrace()
+    for i in range(n_steps):
+        st = spec.steps[i]
+        n = st.n
+        pos = np.concatenate([pos, st.pos.astype(np.int64)])
+        seg = np.concatenate([seg, st.seg])
+        unit = np.concatenate([unit, np.full(n, st.unit, np.int64)])
+        src_step = np.concatenate([src_step, np.full(n, i, np.int64)])
+        src_row = np.concatenate([src_row, np.arange(n, dtype=np.int64)])
+        cur = max(cur, st.unit)
+        tr.peak = max(tr.peak, pos.shape[0])
+        if not evict:
+            tr.steps.append(StepTrace(pos.shape[0], pos.shape[0], [], False, 0))
+            continue
+        plan = plan_eviction(seg, unit, budget, window, cur)
+        keep = ~plan.evict_mask
+        if plan.evict_mask.any():
+            first = int(np.argmax(plan.evict_mask))
+            moved = int(keep[first:].sum())
+        else:
+            moved = 0
+        tr.steps.append(StepTrace(plan.n_pre, plan.n_post, plan.units, plan.budget_unmet, moved))
+        pos, seg, unit = pos[keep], seg[keep], unit[keep]
+        src_step, src_row = src_step[keep], src_row[keep]
+    tr.pos, tr.seg, tr.unit, tr.src_step, tr.src_row = pos, seg, unit, src_step, src_row
+    return tr
+
+
+def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window: int,
+           n_steps: int, layers: Sequence[int]) -> OracleCache:
+    """Oracle cache holding the state of ``spec`` after its first ``n_steps`` steps.
+
+    The surviving rows are re-appended in cache order with their original
+    positions (so their keys get the rotation of those positions), with
+    values regenerated from the seeded generator for ``layers``.
+    """
+    tr = replay_metadata(spec, budget, window, n_steps)
+    cache = OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, layers,
+                        theta=cfg.rope_theta, scale=cfg.scale)
+    # group consecutive survivors by (step) so each appended batch has one unit id
+    steps = tr.src_step
+    starts = np.flatnonzero(np.r_[True, steps[1:] != steps[:-1]])
+    ends = np.r_[starts[1:], steps.shape[0]]
+    for a, b in zip(starts, ends):
+        st = spec.steps[int(steps[a])]
+        vals = step_values(cfg, seed, spec.stream, st.key, st.n, layers)
+        rows = tr.src_row[a:b]
+        k = {l: vals["k"][i][rows] for i, l in enumerate(layers)}
+        v = {l: vals["v"][i][rows] for i, l in enumerate(layers)}
+        cache.append(tr.seg[a:b], tr.pos[a:b], int(tr.unit[a]), k, v)
+    cache.peak = tr.peak
+    # the newest unit and position may belong to rows that were just evicted
+    if n_steps:
+        cache.cur = max(st.unit for st in spec.steps[:n_steps])
+        cache.last_pos = int(spec.steps[n_steps - 1].pos[-1])
+    cache.step_rows = 0
+    return cache
+
