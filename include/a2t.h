@@ -1,0 +1,254 @@
+/*
+ * a2t.h — C ABI of libA2T, the MI355X (gfx950) streaming KV step of
+ * acoustic-to-text KV compression for full-duplex speech models.
+ *
+ * One cache holds, for every layer and every stream, the resident key/value
+ * rows of a duplex session.  Per step (one listening unit, or one decode
+ * token while speaking) the caller
+ *   1. appends the step's rows, layer by layer          (a2t_append),
+ *   2. runs attention for the step's new rows            (a2t_chunk_attn /
+ *                                                         a2t_decode_attn),
+ *   3. after the last layer, evicts under a budget and compacts (a2t_evict).
+ *
+ * Paper passages (Sec. = section of the paper):
+ *   Sec. 3.1  a unit is ~10 audio tokens plus marker and decision; its
+ *             transcript segment, delimited by two ASR tokens, follows the
+ *             first decision and stays in context.
+ *   Sec. 3.3  after each unit, if the resident positions (prefix and text
+ *             included) exceed budget B, evict the acoustic and structural
+ *             rows (unit marker, audio, decision, ASR delimiters, terminators)
+ *             of the oldest unit outside the W most recent units; repeat until
+ *             the cache fits or no eligible unit remains.  Transcript tokens,
+ *             response text and the system prefix are kept.  Position ids
+ *             advance with every fed token whatever is evicted, so kept keys
+ *             keep their rotary positions and are never re-encoded.
+ *
+ * Conventions
+ *   - Return value: A2T_OK (0) or a negative a2t_status.  Every argument is
+ *     validated before any state changes or any work is enqueued, so a call
+ *     that fails changes nothing.
+ *   - "device" pointers are HIP device memory (e.g. torch CUDA tensors on
+ *     ROCm); "host" pointers are ordinary CPU memory, read before the call
+ *     returns.  Device buffers must stay valid until the HIP stream reaches
+ *     the enqueued work; outputs are ready after the stream does.
+ *   - All compute is enqueued on the cache's HIP stream (a2t_set_stream).
+ *     Nothing in a2t_append / a2t_chunk_attn / a2t_decode_attn / a2t_evict
+ *     allocates memory or synchronises the device; the a2t_read_* calls do
+ *     synchronise.
+ *   - A device fault or launch failure poisons the cache: that call and every
+ *     later one return A2T_ERR_HIP.
+ *   - One host thread at a time per cache.
+ *   - Element types: A2T_F32 (float) or A2T_BF16 (bfloat16, raw 16-bit).
+ *     Q, K, V and O all use the cache's dtype; arithmetic is fp32 with
+ *     fp64-accurate rotary angles.
+ *   - Rotary encoding: rotate-half, x'[i] = x[i] cos a - x[i+D/2] sin a,
+ *     x'[i+D/2] = x[i+D/2] cos a + x[i] sin a, a = pos * theta^(-2i/D), i < D/2.
+ *     Query head h reads KV head h / (n_q_heads / n_kv_heads).
+ *   - Causality: a step's query row i sees every resident row up to and
+ *     including itself (the rows of the step are appended before attention).
+ *
+ * Cache order and layout
+ *   The resident rows of a stream are kept in the order they were appended
+ *   (position order).  Eviction removes rows and keeps the survivors in that
+ *   order: survivor i moves to slot new_slot[i] = number of survivors before
+ *   it.  Physically a stream's rows live in two dense regions per layer:
+ *   the "kept" region (rows retained from already-evicted units, in order)
+ *   followed, logically, by a ring of the rows of units not yet evicted.
+ *   Evicting the oldest units advances the ring head and moves only their
+ *   retained rows into the kept region; a2t_read_layout / a2t_read_kv return
+ *   the rows in cache order.
+ */
+#ifndef A2T_H
+#define A2T_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define A2T_ABI_VERSION 1
+#define A2T_ALL_LAYERS (-1)
+
+typedef struct a2t_cache a2t_cache;
+
+typedef enum a2t_status {
+    A2T_OK = 0,
+    A2T_ERR_INVALID = -1,   /* bad argument: null pointer, out-of-range id/size/class */
+    A2T_ERR_POS = -2,       /* position not strictly increasing, unit id decreasing,
+                               or metadata that contradicts the registered step */
+    A2T_ERR_CAPACITY = -3,  /* a region of the cache would overflow */
+    A2T_ERR_STATE = -4,     /* call out of order (layer not appended, step open, ...) */
+    A2T_ERR_OOM = -5,       /* device or pinned-host allocation failed (create only) */
+    A2T_ERR_HIP = -6,       /* HIP runtime error or device fault; the cache is poisoned */
+    A2T_ERR_NODEV = -7      /* no usable gfx950 device, or a host-only cache was asked
+                               for device work */
+} a2t_status;
+
+typedef enum a2t_dtype { A2T_F32 = 0, A2T_BF16 = 1 } a2t_dtype;
+
+/* Row classes (Sec. 3.3).  ACOUSTIC covers every structural state the paper
+ * evicts besides the ASR delimiters: unit marker, audio tokens, native
+ * decision, terminators.  DELIM is the ASR start/end delimiter.  TEXT is a
+ * transcript token, RESPONSE a model-generated response token, PREFIX the
+ * system prefix (unit id -1).  ACOUSTIC and DELIM rows are evictable. */
+typedef enum a2t_seg {
+    A2T_SEG_PREFIX = 0,
+    A2T_SEG_ACOUSTIC = 1,
+    A2T_SEG_DELIM = 2,
+    A2T_SEG_TEXT = 3,
+    A2T_SEG_RESPONSE = 4
+} a2t_seg;
+
+/* Cache creation flags. */
+#define A2T_FLAG_HOST_ONLY 1u  /* no device: bookkeeping and eviction planning only
+                                  (append/evict update the host state; attention and
+                                  device reads return A2T_ERR_NODEV) */
+
+typedef struct a2t_config {
+    int32_t n_layers;       /* L >= 1 */
+    int32_t n_streams;      /* S >= 1 independent sessions */
+    int32_t n_q_heads;      /* Hq, a multiple of n_kv_heads */
+    int32_t n_kv_heads;     /* Hkv >= 1 */
+    int32_t head_dim;       /* D: 64 or 128 */
+    int32_t dtype;          /* a2t_dtype */
+    int32_t unit_rows;      /* per (layer, stream): capacity of the ring of rows of
+                               units not yet evicted */
+    int32_t kept_rows;      /* per (layer, stream): capacity of the region of rows
+                               retained from evicted units (and the prefix) */
+    int32_t max_step_rows;  /* most rows one stream appends in one step (<= 1024) */
+    uint32_t flags;         /* A2T_FLAG_* */
+    double rope_theta;      /* rotary base; 0 selects 1e6 */
+    double attn_scale;      /* softmax scale; 0 selects 1/sqrt(head_dim) */
+    int32_t device;         /* HIP device ordinal */
+    int32_t reserved;
+} a2t_config;
+
+/* Per-stream bookkeeping, for tests and reporting. */
+typedef struct a2t_stream_info {
+    int32_t resident;       /* R: rows in the cache now */
+    int32_t peak;           /* largest R seen right after an append */
+    int32_t kept;           /* rows in the kept region */
+    int32_t ring;           /* rows in the unit ring */
+    int32_t ring_head;      /* ring slot of the oldest not-yet-evicted row */
+    int32_t cur_unit;       /* newest unit id appended (-2 if none) */
+    int32_t last_evicted_unit;  /* newest unit id evicted (-2 if none) */
+    int32_t step_rows;      /* rows of the open step (0 if none) */
+    int64_t last_pos;       /* last position id appended (-1 if none) */
+    int64_t evicted_total;  /* rows evicted since creation */
+    int64_t moved_total;    /* rows copied into the kept region since creation */
+    int32_t budget_unmet;   /* 1 if the last a2t_evict left R > budget */
+    int32_t last_evict_pre; /* R before the last eviction that removed rows (-1 if none) */
+} a2t_stream_info;
+
+/* Create a cache.  Allocates every device buffer it will ever use (K/V pools,
+ * metadata, attention workspace) and a small pinned-host staging area.
+ * hip_stream: the hipStream_t to enqueue on (NULL = the default stream).
+ * Pools hold L*S*Hkv*(unit_rows+kept_rows)*D elements for each of K and V. */
+int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out);
+
+/* Wait for the stream, then free everything the cache owns.  NULL is a no-op. */
+int a2t_cache_destroy(a2t_cache* c);
+
+/* Change the HIP stream later calls enqueue on. */
+int a2t_set_stream(a2t_cache* c, void* hip_stream);
+
+/* Append one step's rows (Sec. 3.1, Sec. 3.3).
+ *   layer       0..L-1, or A2T_ALL_LAYERS.
+ *   stream_ids  host [n_streams], distinct ids in 0..S-1.
+ *   n_rows      host [n_streams], 1..max_step_rows rows per stream.
+ *   k, v        device, pre-rotation, packed in stream order:
+ *               [sum n_rows][Hkv][D] for one layer,
+ *               [L][sum n_rows][Hkv][D] for A2T_ALL_LAYERS.
+ *   seg         host [sum n_rows] a2t_seg per row.
+ *   pos         host [sum n_rows] position ids, strictly increasing within a
+ *               stream and across its steps (gaps allowed), < 2^31.
+ *   unit_id     host [n_streams] unit id of every row of the stream's step:
+ *               -1 for a prefix step (PREFIX rows only), otherwise >= 0 and not
+ *               below the stream's newest unit id.  A decode step repeats the
+ *               newest unit id.
+ * Layer 0 (or A2T_ALL_LAYERS) opens a new step for each listed stream: it
+ * requires the previous step to be appended on every layer, and seg/pos/
+ * unit_id.  Layers 1..L-1 then append the same n_rows; their seg/pos/unit_id
+ * may be NULL (if given they must equal the registered values).
+ * K rows are stored rotated by their position; V rows as given.
+ * Errors: INVALID, POS, CAPACITY (ring full), STATE (layer already appended
+ * this step, or layer 0 before the previous step finished). */
+int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* stream_ids,
+               const int32_t* n_rows, const void* k, const void* v, const uint8_t* seg,
+               const int32_t* pos, const int32_t* unit_id);
+
+/* Causal chunk attention for the step's newest rows (Sec. 3.1: the unit's
+ * tokens are processed over the resident cache).
+ *   n_q   host [n_streams]: queries are the stream's last n_q rows appended
+ *         this step (1 <= n_q <= step rows); their stored positions rotate q.
+ *   q     device [sum n_q][Hq][D], pre-rotation.
+ *   o     device [sum n_q][Hq][D], written with softmax(scale q.K^T) V over the
+ *         resident rows of `layer` up to each query's own row.
+ * The layer must have appended the current step.  Errors: INVALID, STATE. */
+int a2t_chunk_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* stream_ids,
+                   const int32_t* n_q, const void* q, void* o);
+
+/* Decode attention while speaking: one query per stream, the stream's newest
+ * row (Sec. 3.1: response tokens are decoded one by one over the cache).
+ *   q, o  device [n_streams][Hq][D].  Errors as a2t_chunk_attn. */
+int a2t_decode_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* stream_ids,
+                    const void* q, void* o);
+
+/* Online budgeted eviction and compaction after a step (Sec. 3.3).
+ * For each listed stream: while R > budget[i] and some unit u <= cur - window
+ * still holds ACOUSTIC/DELIM rows, remove every ACOUSTIC/DELIM row of the
+ * oldest such unit.  Survivors keep their positions and order.  One pass
+ * moves the retained rows of all evicted units, in every layer.
+ *   budget       host [n_streams], >= 0.
+ *   window       recent units protected (cur-window+1 .. cur), >= 0.
+ *   n_evicted    optional host [n_streams] out: rows removed.
+ *   budget_unmet optional host [n_streams] out: 1 if R > budget afterwards.
+ * Requires every layer to have appended the stream's step.  A budget that
+ * cannot be met is not an error.  Errors: INVALID, STATE, CAPACITY (kept
+ * region full). */
+int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* stream_ids, const int32_t* budget,
+              int32_t window, int32_t* n_evicted, uint8_t* budget_unmet);
+
+/* Bookkeeping of one stream (host state, no synchronisation). */
+int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out);
+
+/* Copy one stream's layout to host, in cache order (synchronises).
+ * pos, seg, unit: host [resident] (any may be NULL).  The values are read from
+ * the device metadata, not from the host state. */
+int a2t_read_layout(a2t_cache* c, int32_t stream, int32_t* pos, uint8_t* seg, int32_t* unit);
+
+/* The device-computed result of the stream's last eviction that removed rows
+ * (synchronises).  n_pre: rows before it.  mask: host [n_pre], 1 = evicted.
+ * new_slot: host [n_pre], survivor index or -1.  Either array may be NULL.
+ * Returns A2T_ERR_STATE if the stream never evicted. */
+int a2t_read_last_evict(a2t_cache* c, int32_t stream, int32_t* n_pre, uint8_t* mask,
+                        int32_t* new_slot);
+
+/* Copy one layer's resident K (rotated) and V of a stream to host in cache
+ * order (synchronises).  k, v: host [resident][Hkv][D] in the cache dtype. */
+int a2t_read_kv(a2t_cache* c, int32_t layer, int32_t stream, void* k, void* v);
+
+/* Wait for all work enqueued by this cache.  Reports device faults. */
+int a2t_sync(a2t_cache* c);
+
+/* Kernel timing with HIP events on the cache's stream (for benchmarks).
+ * kernel_filter: NULL disables timing; "" times every kernel; otherwise only
+ * kernels whose name contains the string ("step_meta", "append",
+ * "attn_mfma", "attn_valu", "attn_merge", "evict").  While enabled, each
+ * matching launch is bracketed by two events.  a2t_kernel_time waits for the
+ * stream, then reports for the kernels whose name contains `kernel` the
+ * number of launches and their summed duration in milliseconds since the
+ * last report, and resets those counters. */
+int a2t_profile_enable(a2t_cache* c, const char* kernel_filter);
+int a2t_kernel_time(a2t_cache* c, const char* kernel, int64_t* launches, double* total_ms);
+
+/* Static strings. */
+const char* a2t_status_str(int status);
+int a2t_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* A2T_H */

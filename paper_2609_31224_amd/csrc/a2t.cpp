@@ -1,0 +1,851 @@
+// libA2T host side: argument validation, the per-stream host state, the
+// eviction planner of Sec. 3.3, and kernel launches.  Public API: include/a2t.h.
+//
+// The host state mirrors what the device holds, so no call needs to read the
+// device back to plan work: per stream it knows the kept-region size, the
+// ring head and size, and the queue of not-yet-evicted units with their row
+// counts.  Eviction is planned from those counts (positions are what the
+// paper's budget counts) and the device then derives the per-row mask,
+// compaction indices and row moves itself.
+#include "../../include/a2t.h"
+#include "a2t_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <deque>
+#include <map>
+#include <string>
+#include <vector>
+
+using namespace a2t;
+
+namespace {
+
+struct UnitRec {
+    int32_t unit;
+    int32_t rows;       // rows of this unit still in the ring
+    int32_t evictable;  // ACOUSTIC/DELIM rows among them
+};
+
+struct StreamState {
+    int64_t last_pos = -1;
+    int32_t cur_unit = -2;          // -2: nothing appended yet
+    int32_t last_evicted = -2;
+    int32_t kept = 0;               // T
+    int32_t head = 0;               // ring head slot
+    int32_t ring = 0;               // U
+    int32_t peak = 0;
+    std::deque<UnitRec> units;
+    // open step
+    int32_t step_rows = 0;
+    int32_t step_slot0 = 0;
+    std::vector<uint8_t> appended;  // per layer, for the open step
+    std::vector<uint8_t> step_seg;
+    std::vector<int32_t> step_pos;
+    int32_t step_unit = 0;
+    // stats
+    int64_t evicted_total = 0;
+    int64_t moved_total = 0;
+    int32_t budget_unmet = 0;
+    int32_t last_evict_pre = -1;
+
+    int32_t resident() const { return kept + ring; }
+    bool step_complete() const {
+        for (uint8_t a : appended)
+            if (!a) return false;
+        return true;
+    }
+};
+
+struct ProfEvent {
+    std::string name;
+    hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct a2t_cache {
+    a2t_config cfg{};
+    bool host_only = false;
+    hipStream_t stream = nullptr;
+    int poisoned = 0;
+    DevState dev{};
+    std::vector<StreamState> ss;
+    // pinned staging slots for step metadata, reused round-robin behind events
+    uint8_t* stage = nullptr;      // host address
+    uint8_t* stage_dev = nullptr;  // the same memory as seen by kernels
+    size_t slot_bytes = 0;
+    int n_slots = 0;
+    int next_slot = 0;
+    std::vector<hipEvent_t> slot_ev;
+    std::vector<uint8_t> slot_live;
+    // attention tuning
+    int target_wgs = 1024;
+    int force_splits = 0;
+    bool force_valu = false;
+    // profiling
+    bool prof_on = false;
+    std::string prof_filter;
+    std::deque<ProfEvent> prof_pending;
+    std::vector<hipEvent_t> prof_free;
+    std::map<std::string, std::pair<int64_t, double>> prof_acc;
+};
+
+namespace {
+
+int hip_fail(a2t_cache* c) {
+    if (c) c->poisoned = 1;
+    return A2T_ERR_HIP;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    bool changed = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) {
+            changed = hipSetDevice(dev) == hipSuccess;
+        }
+    }
+    ~DeviceGuard() {
+        if (changed) (void)hipSetDevice(prev);
+    }
+};
+
+bool env_flag(const char* name) {
+    const char* v = std::getenv(name);
+    return v && *v && std::strcmp(v, "0") != 0;
+}
+int env_int(const char* name, int dflt) {
+    const char* v = std::getenv(name);
+    return (v && *v) ? std::atoi(v) : dflt;
+}
+
+// ---- profiling ---------------------------------------------------------------
+void prof_harvest(a2t_cache* c, bool wait) {
+    while (!c->prof_pending.empty()) {
+        ProfEvent& e = c->prof_pending.front();
+        if (wait) {
+            if (hipEventSynchronize(e.stop) != hipSuccess) return;
+        } else if (hipEventQuery(e.stop) != hipSuccess) {
+            return;
+        }
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, e.start, e.stop) == hipSuccess) {
+            auto& acc = c->prof_acc[e.name];
+            acc.first += 1;
+            acc.second += ms;
+        }
+        c->prof_free.push_back(e.start);
+        c->prof_free.push_back(e.stop);
+        c->prof_pending.pop_front();
+    }
+}
+
+struct ProfScope {
+    a2t_cache* c;
+    ProfEvent ev;
+    bool on = false;
+    ProfScope(a2t_cache* cc, const char* name) : c(cc) {
+        if (!c->prof_on) return;
+        if (!c->prof_filter.empty() && std::strstr(name, c->prof_filter.c_str()) == nullptr) return;
+        prof_harvest(c, false);
+        if (c->prof_free.size() < 2) {
+            hipEvent_t a, b;
+            if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
+            c->prof_free.push_back(a);
+            c->prof_free.push_back(b);
+        }
+        ev.name = name;
+        ev.stop = c->prof_free.back();
+        c->prof_free.pop_back();
+        ev.start = c->prof_free.back();
+        c->prof_free.pop_back();
+        on = hipEventRecord(ev.start, c->stream) == hipSuccess;
+    }
+    ~ProfScope() {
+        if (!on) return;
+        if (hipEventRecord(ev.stop, c->stream) == hipSuccess) c->prof_pending.push_back(ev);
+    }
+};
+
+// ---- staging -------------------------------------------------------------------
+uint8_t* stage_acquire(a2t_cache* c, int* slot_out) {
+    const int s = c->next_slot;
+    c->next_slot = (c->next_slot + 1) % c->n_slots;
+    if (c->slot_live[s]) {
+        if (hipEventSynchronize(c->slot_ev[s]) != hipSuccess) return nullptr;
+        c->slot_live[s] = 0;
+    }
+    *slot_out = s;
+    return c->stage + (size_t)s * c->slot_bytes;
+}
+bool stage_release(a2t_cache* c, int slot) {
+    if (hipEventRecord(c->slot_ev[slot], c->stream) != hipSuccess) return false;
+    c->slot_live[slot] = 1;
+    return true;
+}
+
+int check_streams(const a2t_cache* c, int32_t n, const int32_t* ids) {
+    if (n < 1 || n > c->cfg.n_streams || !ids) return A2T_ERR_INVALID;
+    std::vector<uint8_t> seen(c->cfg.n_streams, 0);
+    for (int i = 0; i < n; ++i) {
+        if (ids[i] < 0 || ids[i] >= c->cfg.n_streams || seen[ids[i]]) return A2T_ERR_INVALID;
+        seen[ids[i]] = 1;
+    }
+    return A2T_OK;
+}
+
+bool is_evictable(uint8_t seg) { return seg == A2T_SEG_ACOUSTIC || seg == A2T_SEG_DELIM; }
+
+// Splits of the key range for one attention launch.
+int choose_splits(const a2t_cache* c, int n_desc, int max_R, int64_t floats_per_split_all) {
+    const int n_tiles = std::max(1, (max_R + kTileKeys - 1) / kTileKeys);
+    int sp;
+    if (c->force_splits > 0) {
+        sp = c->force_splits;
+    } else {
+        const int per = n_desc * c->cfg.n_kv_heads;
+        sp = std::max(1, (c->target_wgs + per - 1) / per);
+        // keep at least two tiles per split unless forced
+        sp = std::min(sp, std::max(1, n_tiles / 2));
+    }
+    sp = std::min(sp, n_tiles);
+    if (sp > 1) {
+        const int64_t cap = c->dev.ws_floats / std::max<int64_t>(1, floats_per_split_all);
+        sp = (int)std::min<int64_t>(sp, std::max<int64_t>(1, cap));
+    }
+    return std::max(1, sp);
+}
+
+// One attention launch (plus merge) over up to kMaxDesc streams.
+int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_t* n_q,
+                const int32_t* q_row0, const void* q, void* o, bool decode) {
+    AttnBatch b{};
+    b.count = n;
+    b.layer = layer;
+    const int G = c->cfg.n_q_heads / c->cfg.n_kv_heads;
+    int max_R = 0, max_rows = 0;
+    int64_t floats_all = 0;
+    for (int i = 0; i < n; ++i) {
+        const StreamState& s = c->ss[ids[i]];
+        max_R = std::max(max_R, s.resident());
+        max_rows = std::max(max_rows, n_q[i]);
+        floats_all += (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
+    }
+    const int splits = choose_splits(c, n, max_R, floats_all);
+    int64_t off = 0;
+    for (int i = 0; i < n; ++i) {
+        const StreamState& s = c->ss[ids[i]];
+        AttnDesc& d = b.d[i];
+        d.s = ids[i];
+        d.kept = s.kept;
+        d.head = s.head;
+        d.R = s.resident();
+        d.n_q = n_q[i];
+        d.q_row0 = q_row0[i];
+        d.rope_row0 = s.step_rows - n_q[i];
+        const int n_tiles = (d.R + kTileKeys - 1) / kTileKeys;
+        d.splits = std::max(1, std::min(splits, n_tiles));
+        d.ws_off = off;
+        if (d.splits > 1) off += (int64_t)d.splits * c->cfg.n_kv_heads * G * d.n_q * (c->cfg.head_dim + 2);
+    }
+    b.max_splits = splits;
+    b.max_rows = max_rows;
+    const bool valu = decode || c->cfg.dtype == A2T_F32 || c->force_valu;
+    hipError_t e;
+    {
+        ProfScope ps(c, valu ? "attn_valu" : "attn_mfma");
+        e = valu ? launch_attn_valu(c->dev, b, q, o, c->stream)
+                 : launch_attn_mfma(c->dev, b, q, o, c->stream);
+    }
+    if (e != hipSuccess) return hip_fail(c);
+    if (splits > 1) {
+        ProfScope ps(c, "attn_merge");
+        if (launch_attn_merge(c->dev, b, o, c->stream) != hipSuccess) return hip_fail(c);
+    }
+    return A2T_OK;
+}
+
+int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                const int32_t* n_q, const void* q, void* o, bool decode) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
+    int rc = check_streams(c, n_streams, ids);
+    if (rc) return rc;
+    if (!q || !o || (!decode && !n_q)) return A2T_ERR_INVALID;
+    std::vector<int32_t> nq(n_streams), row0(n_streams);
+    int32_t acc = 0;
+    for (int i = 0; i < n_streams; ++i) {
+        const StreamState& s = c->ss[ids[i]];
+        nq[i] = decode ? 1 : n_q[i];
+        if (nq[i] < 1) return A2T_ERR_INVALID;
+        if (s.step_rows == 0 || !s.appended[layer]) return A2T_ERR_STATE;
+        if (nq[i] > s.step_rows) return A2T_ERR_STATE;
+        row0[i] = acc;
+        acc += nq[i];
+    }
+    if (c->host_only) return A2T_ERR_NODEV;
+    DeviceGuard dg(c->cfg.device);
+    for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
+        const int n = std::min(kMaxDesc, n_streams - i0);
+        rc = attn_launch(c, layer, n, ids + i0, nq.data() + i0, row0.data() + i0, q, o, decode);
+        if (rc) return rc;
+    }
+    return A2T_OK;
+}
+
+void free_device(a2t_cache* c) {
+    void* ptrs[] = {c->dev.k_unit, c->dev.v_unit, c->dev.k_kept, c->dev.v_kept,
+                    c->dev.unit_pos, c->dev.unit_uid, c->dev.unit_seg, c->dev.kept_pos,
+                    c->dev.kept_uid, c->dev.kept_seg, c->dev.rope, c->dev.ev_mask,
+                    c->dev.ev_slot, c->dev.ws};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    if (c->stage) (void)hipHostFree(c->stage);
+    for (hipEvent_t e : c->slot_ev) (void)hipEventDestroy(e);
+    for (auto& e : c->prof_pending) {
+        (void)hipEventDestroy(e.start);
+        (void)hipEventDestroy(e.stop);
+    }
+    for (hipEvent_t e : c->prof_free) (void)hipEventDestroy(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int a2t_abi_version(void) { return A2T_ABI_VERSION; }
+
+const char* a2t_status_str(int status) {
+    switch (status) {
+        case A2T_OK: return "ok";
+        case A2T_ERR_INVALID: return "invalid argument";
+        case A2T_ERR_POS: return "position/unit order or metadata mismatch";
+        case A2T_ERR_CAPACITY: return "cache region capacity exceeded";
+        case A2T_ERR_STATE: return "call out of order";
+        case A2T_ERR_OOM: return "out of memory";
+        case A2T_ERR_HIP: return "HIP error or device fault (cache poisoned)";
+        case A2T_ERR_NODEV: return "no usable gfx950 device";
+        default: return "unknown status";
+    }
+}
+
+int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
+    if (!cfg || !out) return A2T_ERR_INVALID;
+    *out = nullptr;
+    const a2t_config& k = *cfg;
+    if (k.n_layers < 1 || k.n_streams < 1 || k.n_kv_heads < 1 || k.n_q_heads < 1) return A2T_ERR_INVALID;
+    if (k.n_q_heads % k.n_kv_heads) return A2T_ERR_INVALID;
+    const int G = k.n_q_heads / k.n_kv_heads;
+    if (G != 1 && G != 2 && G != 4 && G != 8) return A2T_ERR_INVALID;
+    if (k.head_dim != 64 && k.head_dim != 128) return A2T_ERR_INVALID;
+    if (k.dtype != A2T_F32 && k.dtype != A2T_BF16) return A2T_ERR_INVALID;
+    if (k.unit_rows < 1 || k.kept_rows < 0) return A2T_ERR_INVALID;
+    if (k.max_step_rows < 1 || k.max_step_rows > 1024) return A2T_ERR_INVALID;
+    if (k.rope_theta < 0 || k.attn_scale < 0) return A2T_ERR_INVALID;
+    if ((int64_t)k.unit_rows + k.kept_rows > (int64_t)1 << 30) return A2T_ERR_INVALID;
+
+    a2t_cache* c = new (std::nothrow) a2t_cache();
+    if (!c) return A2T_ERR_OOM;
+    c->cfg = k;
+    if (c->cfg.rope_theta == 0) c->cfg.rope_theta = 1.0e6;
+    if (c->cfg.attn_scale == 0) c->cfg.attn_scale = 1.0 / std::sqrt((double)k.head_dim);
+    c->host_only = (k.flags & A2T_FLAG_HOST_ONLY) != 0;
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    c->ss.resize(k.n_streams);
+    for (auto& s : c->ss) s.appended.assign(k.n_layers, 1);
+    c->target_wgs = std::max(1, env_int("A2T_TARGET_WGS", 1024));
+    c->force_splits = std::max(0, env_int("A2T_SPLITS", 0));
+    c->force_valu = env_flag("A2T_FORCE_VALU");
+
+    DevState& d = c->dev;
+    d.L = k.n_layers;
+    d.S = k.n_streams;
+    d.Hq = k.n_q_heads;
+    d.Hkv = k.n_kv_heads;
+    d.D = k.head_dim;
+    d.dtype = k.dtype;
+    d.unit_rows = k.unit_rows;
+    d.kept_rows = k.kept_rows;
+    d.max_step_rows = k.max_step_rows;
+    d.theta = c->cfg.rope_theta;
+    d.scale_log2e = (float)(c->cfg.attn_scale * 1.4426950408889634);
+    if (c->host_only) {
+        *out = c;
+        return A2T_OK;
+    }
+
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || k.device < 0 || k.device >= ndev) {
+        delete c;
+        return A2T_ERR_NODEV;
+    }
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, k.device) != hipSuccess ||
+        std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+        delete c;
+        return A2T_ERR_NODEV;
+    }
+    DeviceGuard dg(k.device);
+    const int64_t elt = k.dtype == A2T_F32 ? 4 : 2;
+    const int64_t lsh = (int64_t)k.n_layers * k.n_streams * k.n_kv_heads * k.head_dim * elt;
+    const int64_t S = k.n_streams;
+    const int64_t tot = (int64_t)k.unit_rows + k.kept_rows;
+    // workspace: enough for full splitting of one launch of every stream's max step
+    int64_t ws = (int64_t)env_int("A2T_WS_MB", 256) << 20;
+    bool ok = true;
+    auto alloc = [&](void** p, int64_t bytes) {
+        if (!ok) return;
+        if (hipMalloc(p, std::max<int64_t>(bytes, 256)) != hipSuccess) ok = false;
+    };
+    alloc(&d.k_unit, lsh * k.unit_rows);
+    alloc(&d.v_unit, lsh * k.unit_rows);
+    alloc(&d.k_kept, lsh * std::max(1, k.kept_rows));
+    alloc(&d.v_kept, lsh * std::max(1, k.kept_rows));
+    alloc((void**)&d.unit_pos, S * k.unit_rows * 4);
+    alloc((void**)&d.unit_uid, S * k.unit_rows * 4);
+    alloc((void**)&d.unit_seg, S * k.unit_rows);
+    alloc((void**)&d.kept_pos, S * std::max(1, k.kept_rows) * 4);
+    alloc((void**)&d.kept_uid, S * std::max(1, k.kept_rows) * 4);
+    alloc((void**)&d.kept_seg, S * std::max(1, k.kept_rows));
+    alloc((void**)&d.rope, S * k.max_step_rows * (k.head_dim / 2) * 8);
+    alloc((void**)&d.ev_mask, S * tot);
+    alloc((void**)&d.ev_slot, S * tot * 4);
+    alloc((void**)&d.ws, ws);
+    d.ws_floats = ws / 4;
+    // staging: per slot, seg (u8) + pos (i32) for every stream's max step, + unit ids
+    c->n_slots = 16;
+    c->slot_bytes = (size_t)S * k.max_step_rows * 5 + (size_t)kMaxDesc * 4 * ((S + kMaxDesc - 1) / kMaxDesc) + 256;
+    c->slot_bytes = (c->slot_bytes + 255) & ~(size_t)255;
+    if (ok && hipHostMalloc((void**)&c->stage, c->slot_bytes * c->n_slots,
+                            hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
+        c->stage = nullptr;
+        ok = false;
+    }
+    if (ok && hipHostGetDevicePointer((void**)&c->stage_dev, c->stage, 0) != hipSuccess) ok = false;
+    c->slot_ev.resize(c->n_slots, nullptr);
+    c->slot_live.assign(c->n_slots, 0);
+    for (int i = 0; ok && i < c->n_slots; ++i)
+        if (hipEventCreateWithFlags(&c->slot_ev[i], hipEventDisableTiming) != hipSuccess) ok = false;
+    if (!ok) {
+        free_device(c);
+        delete c;
+        (void)hipGetLastError();
+        return A2T_ERR_OOM;
+    }
+    *out = c;
+    return A2T_OK;
+}
+
+int a2t_cache_destroy(a2t_cache* c) {
+    if (!c) return A2T_OK;
+    if (!c->host_only) {
+        DeviceGuard dg(c->cfg.device);
+        (void)hipStreamSynchronize(c->stream);
+        free_device(c);
+    }
+    delete c;
+    return A2T_OK;
+}
+
+int a2t_set_stream(a2t_cache* c, void* hip_stream) {
+    if (!c) return A2T_ERR_INVALID;
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    return A2T_OK;
+}
+
+int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+               const int32_t* n_rows, const void* kin, const void* vin, const uint8_t* seg,
+               const int32_t* pos, const int32_t* unit_id) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    const a2t_config& k = c->cfg;
+    if (layer < A2T_ALL_LAYERS || layer >= k.n_layers) return A2T_ERR_INVALID;
+    int rc = check_streams(c, n_streams, ids);
+    if (rc) return rc;
+    if (!n_rows) return A2T_ERR_INVALID;
+    if (!c->host_only && (!kin || !vin)) return A2T_ERR_INVALID;
+    const bool opens = (layer == 0 || layer == A2T_ALL_LAYERS);
+    if (opens && (!seg || !pos || !unit_id)) return A2T_ERR_INVALID;
+
+    int64_t total = 0;
+    for (int i = 0; i < n_streams; ++i) {
+        if (n_rows[i] < 1 || n_rows[i] > k.max_step_rows) return A2T_ERR_INVALID;
+        total += n_rows[i];
+    }
+    // validate every stream before touching any state
+    int64_t off = 0;
+    for (int i = 0; i < n_streams; ++i) {
+        const StreamState& s = c->ss[ids[i]];
+        const int n = n_rows[i];
+        if (opens) {
+            if (!s.step_complete()) return A2T_ERR_STATE;
+            const int u = unit_id[i];
+            if (u < -1) return A2T_ERR_INVALID;
+            int64_t last = s.last_pos;
+            for (int r = 0; r < n; ++r) {
+                const uint8_t sg = seg[off + r];
+                if (sg > A2T_SEG_RESPONSE) return A2T_ERR_INVALID;
+                if (pos[off + r] < 0) return A2T_ERR_INVALID;
+                if ((u == -1) != (sg == A2T_SEG_PREFIX)) return A2T_ERR_INVALID;
+                if ((int64_t)pos[off + r] <= last) return A2T_ERR_POS;
+                last = pos[off + r];
+            }
+            if (u == -1 && s.cur_unit >= 0) return A2T_ERR_POS;
+            if (s.cur_unit != -2 && u < s.cur_unit) return A2T_ERR_POS;
+            if ((int64_t)s.ring + n > k.unit_rows) return A2T_ERR_CAPACITY;
+        } else {
+            if (s.step_rows == 0 || s.appended[layer]) return A2T_ERR_STATE;
+            if (n != s.step_rows) return A2T_ERR_POS;
+            if (seg || pos) {
+                for (int r = 0; r < n; ++r) {
+                    if (seg && seg[off + r] != s.step_seg[r]) return A2T_ERR_POS;
+                    if (pos && pos[off + r] != s.step_pos[r]) return A2T_ERR_POS;
+                }
+            }
+            if (unit_id && unit_id[i] != s.step_unit) return A2T_ERR_POS;
+        }
+        off += n;
+    }
+
+    // state update
+    off = 0;
+    for (int i = 0; i < n_streams; ++i) {
+        StreamState& s = c->ss[ids[i]];
+        const int n = n_rows[i];
+        if (opens) {
+            const int u = unit_id[i];
+            int ev = 0;
+            for (int r = 0; r < n; ++r) ev += is_evictable(seg[off + r]);
+            s.step_rows = n;
+            s.step_slot0 = (s.head + s.ring) % k.unit_rows;
+            s.step_seg.assign(seg + off, seg + off + n);
+            s.step_pos.assign(pos + off, pos + off + n);
+            s.step_unit = u;
+            std::fill(s.appended.begin(), s.appended.end(), layer == A2T_ALL_LAYERS ? 1 : 0);
+            if (layer == 0) s.appended[0] = 1;
+            s.ring += n;
+            if (!s.units.empty() && s.units.back().unit == u) {
+                s.units.back().rows += n;
+                s.units.back().evictable += ev;
+            } else {
+                s.units.push_back(UnitRec{u, n, ev});
+            }
+            s.cur_unit = std::max(s.cur_unit, u);
+            s.last_pos = pos[off + n - 1];
+            s.peak = std::max(s.peak, s.resident());
+            s.budget_unmet = 0;
+        } else {
+            s.appended[layer] = 1;
+        }
+        off += n;
+    }
+    if (c->host_only) return A2T_OK;
+
+    DeviceGuard dg(k.device);
+    // 1. step registration: metadata + rotary table (once per step)
+    if (opens) {
+        int64_t row = 0;
+        for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
+            const int n = std::min(kMaxDesc, n_streams - i0);
+            int slot;
+            uint8_t* sp = stage_acquire(c, &slot);
+            if (!sp) return hip_fail(c);
+            StepBatch sb{};
+            sb.count = n;
+            int64_t rows_here = 0;
+            for (int i = 0; i < n; ++i) rows_here += n_rows[i0 + i];
+            int32_t* spos = reinterpret_cast<int32_t*>(sp);
+            int32_t* suid = spos + rows_here;
+            uint8_t* sseg = reinterpret_cast<uint8_t*>(suid + n);
+            std::memcpy(spos, pos + row, rows_here * 4);
+            std::memcpy(sseg, seg + row, rows_here);
+            int64_t r0 = 0;
+            for (int i = 0; i < n; ++i) {
+                const StreamState& s = c->ss[ids[i0 + i]];
+                sb.d[i] = StepDesc{ids[i0 + i], n_rows[i0 + i], s.step_slot0, (int32_t)r0};
+                suid[i] = unit_id[i0 + i];
+                r0 += n_rows[i0 + i];
+            }
+            const ptrdiff_t shift = c->stage_dev - c->stage;
+            hipError_t e;
+            {
+                ProfScope ps(c, "step_meta");
+                e = launch_step_meta(c->dev, sb, reinterpret_cast<const uint8_t*>(sseg) + shift,
+                                     reinterpret_cast<const int32_t*>(reinterpret_cast<uint8_t*>(spos) + shift),
+                                     reinterpret_cast<const int32_t*>(reinterpret_cast<uint8_t*>(suid) + shift),
+                                     c->stream);
+            }
+            if (e != hipSuccess || !stage_release(c, slot)) return hip_fail(c);
+            row += rows_here;
+        }
+    }
+    // 2. rotate and store K, store V
+    {
+        int64_t in_row = 0;
+        for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
+            const int n = std::min(kMaxDesc, n_streams - i0);
+            AppendBatch ab{};
+            ab.count = n;
+            ab.layer0 = layer == A2T_ALL_LAYERS ? 0 : layer;
+            ab.total_rows = (int32_t)total;
+            int max_n = 0;
+            for (int i = 0; i < n; ++i) {
+                const StreamState& s = c->ss[ids[i0 + i]];
+                ab.d[i] = AppendDesc{ids[i0 + i], n_rows[i0 + i], s.step_slot0, (int32_t)in_row};
+                in_row += n_rows[i0 + i];
+                max_n = std::max(max_n, n_rows[i0 + i]);
+            }
+            ab.max_n = max_n;
+            hipError_t e;
+            {
+                ProfScope ps(c, "append");
+                e = launch_append(c->dev, ab, layer == A2T_ALL_LAYERS ? k.n_layers : 1, kin, vin,
+                                  c->stream);
+            }
+            if (e != hipSuccess) return hip_fail(c);
+        }
+    }
+    return A2T_OK;
+}
+
+int a2t_chunk_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                   const int32_t* n_q, const void* q, void* o) {
+    return attn_common(c, layer, n_streams, ids, n_q, q, o, false);
+}
+
+int a2t_decode_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                    const void* q, void* o) {
+    return attn_common(c, layer, n_streams, ids, nullptr, q, o, true);
+}
+
+int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t* budget,
+              int32_t window, int32_t* n_evicted, uint8_t* budget_unmet) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    int rc = check_streams(c, n_streams, ids);
+    if (rc) return rc;
+    if (!budget || window < 0) return A2T_ERR_INVALID;
+    struct Plan {
+        int n_units = 0;      // units popped from the ring queue (passed over or evicted)
+        int32_t span = 0, n_keep = 0, evicted = 0, u_last = -2, R_pre = 0;
+        bool unmet = false;
+    };
+    std::vector<Plan> plans(n_streams);
+    for (int i = 0; i < n_streams; ++i) {
+        if (budget[i] < 0) return A2T_ERR_INVALID;
+        const StreamState& s = c->ss[ids[i]];
+        if (!s.step_complete()) return A2T_ERR_STATE;
+        // Sec. 3.3: while R > B, evict the oldest unit outside the W most recent
+        // units that still holds acoustic/structural rows.
+        Plan& p = plans[i];
+        int32_t R = s.resident();
+        p.R_pre = R;
+        const int64_t limit = (int64_t)s.cur_unit - window;
+        size_t next = 0;
+        while (R > budget[i]) {
+            size_t j = next;
+            while (j < s.units.size() && s.units[j].evictable == 0) ++j;
+            if (j >= s.units.size() || (int64_t)s.units[j].unit > limit) break;
+            for (size_t t = next; t <= j; ++t) {
+                p.span += s.units[t].rows;
+                p.n_keep += s.units[t].rows - s.units[t].evictable;
+            }
+            p.evicted += s.units[j].evictable;
+            R -= s.units[j].evictable;
+            p.u_last = s.units[j].unit;
+            next = j + 1;
+        }
+        p.n_units = (int)next;
+        p.unmet = R > budget[i];
+        if ((int64_t)s.kept + p.n_keep > c->cfg.kept_rows) return A2T_ERR_CAPACITY;
+    }
+    // device work for the streams that evict
+    if (!c->host_only) {
+        DeviceGuard dg(c->cfg.device);
+        EvictBatch eb{};
+        auto flush = [&]() -> int {
+            if (eb.count == 0) return A2T_OK;
+            hipError_t e;
+            {
+                ProfScope ps(c, "evict");
+                e = launch_evict(c->dev, eb, c->stream);
+            }
+            eb.count = 0;
+            return e == hipSuccess ? A2T_OK : hip_fail(c);
+        };
+        for (int i = 0; i < n_streams; ++i) {
+            const Plan& p = plans[i];
+            if (p.evicted == 0) continue;
+            const StreamState& s = c->ss[ids[i]];
+            eb.d[eb.count++] = EvictDesc{ids[i], s.kept, s.head, p.R_pre, p.span, p.u_last, p.n_keep};
+            if (eb.count == kMaxDesc && (rc = flush())) return rc;
+        }
+        if ((rc = flush())) return rc;
+    }
+    // host state
+    for (int i = 0; i < n_streams; ++i) {
+        StreamState& s = c->ss[ids[i]];
+        const Plan& p = plans[i];
+        if (p.evicted > 0) {
+            for (int t = 0; t < p.n_units; ++t) s.units.pop_front();
+            s.kept += p.n_keep;
+            s.head = (int32_t)(((int64_t)s.head + p.span) % c->cfg.unit_rows);
+            s.ring -= p.span;
+            s.last_evicted = p.u_last;
+            s.evicted_total += p.evicted;
+            s.moved_total += p.n_keep;
+            s.last_evict_pre = p.R_pre;
+        }
+        s.budget_unmet = p.unmet ? 1 : 0;
+        s.step_rows = 0;
+        std::fill(s.appended.begin(), s.appended.end(), 1);
+        if (n_evicted) n_evicted[i] = p.evicted;
+        if (budget_unmet) budget_unmet[i] = p.unmet ? 1 : 0;
+    }
+    return A2T_OK;
+}
+
+int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out) {
+    if (!c || !out || stream < 0 || stream >= c->cfg.n_streams) return A2T_ERR_INVALID;
+    const StreamState& s = c->ss[stream];
+    out->resident = s.resident();
+    out->peak = s.peak;
+    out->kept = s.kept;
+    out->ring = s.ring;
+    out->ring_head = s.head;
+    out->cur_unit = s.cur_unit;
+    out->last_evicted_unit = s.last_evicted;
+    out->step_rows = s.step_rows;
+    out->last_pos = s.last_pos;
+    out->evicted_total = s.evicted_total;
+    out->moved_total = s.moved_total;
+    out->budget_unmet = s.budget_unmet;
+    out->last_evict_pre = s.last_evict_pre;
+    return A2T_OK;
+}
+
+int a2t_sync(a2t_cache* c) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_OK;
+    if (c->poisoned) return A2T_ERR_HIP;
+    DeviceGuard dg(c->cfg.device);
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return hip_fail(c);
+    if (hipGetLastError() != hipSuccess) return hip_fail(c);
+    return A2T_OK;
+}
+
+int a2t_read_layout(a2t_cache* c, int32_t stream, int32_t* pos, uint8_t* seg, int32_t* unit) {
+    if (!c || stream < 0 || stream >= c->cfg.n_streams) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    int rc = a2t_sync(c);
+    if (rc) return rc;
+    DeviceGuard dg(c->cfg.device);
+    const StreamState& s = c->ss[stream];
+    const int64_t kb = (int64_t)stream * c->cfg.kept_rows, ub = (int64_t)stream * c->cfg.unit_rows;
+    const int T = s.kept, U = s.ring, head = s.head, cap = c->cfg.unit_rows;
+    const int first = std::min(U, cap - head), second = U - first;
+    auto get = [&](void* dst, const void* src_kept, const void* src_ring, size_t elt) -> bool {
+        if (!dst) return true;
+        char* d = static_cast<char*>(dst);
+        const char* sk = static_cast<const char*>(src_kept) + kb * elt;
+        const char* sr = static_cast<const char*>(src_ring) + ub * elt;
+        if (T && hipMemcpy(d, sk, T * elt, hipMemcpyDeviceToHost) != hipSuccess) return false;
+        if (first && hipMemcpy(d + T * elt, sr + head * elt, first * elt, hipMemcpyDeviceToHost) != hipSuccess) return false;
+        if (second && hipMemcpy(d + (T + first) * elt, sr, second * elt, hipMemcpyDeviceToHost) != hipSuccess) return false;
+        return true;
+    };
+    if (!get(pos, c->dev.kept_pos, c->dev.unit_pos, 4) || !get(seg, c->dev.kept_seg, c->dev.unit_seg, 1) ||
+        !get(unit, c->dev.kept_uid, c->dev.unit_uid, 4))
+        return hip_fail(c);
+    return A2T_OK;
+}
+
+int a2t_read_last_evict(a2t_cache* c, int32_t stream, int32_t* n_pre, uint8_t* mask,
+                        int32_t* new_slot) {
+    if (!c || stream < 0 || stream >= c->cfg.n_streams) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    const StreamState& s = c->ss[stream];
+    if (s.last_evict_pre < 0) return A2T_ERR_STATE;
+    int rc = a2t_sync(c);
+    if (rc) return rc;
+    DeviceGuard dg(c->cfg.device);
+    const int64_t eb = (int64_t)stream * ((int64_t)c->cfg.unit_rows + c->cfg.kept_rows);
+    const int n = s.last_evict_pre;
+    if (n_pre) *n_pre = n;
+    if (mask && hipMemcpy(mask, c->dev.ev_mask + eb, n, hipMemcpyDeviceToHost) != hipSuccess) return hip_fail(c);
+    if (new_slot && hipMemcpy(new_slot, c->dev.ev_slot + eb, (size_t)n * 4, hipMemcpyDeviceToHost) != hipSuccess)
+        return hip_fail(c);
+    return A2T_OK;
+}
+
+int a2t_read_kv(a2t_cache* c, int32_t layer, int32_t stream, void* kout, void* vout) {
+    if (!c || stream < 0 || stream >= c->cfg.n_streams || layer < 0 || layer >= c->cfg.n_layers)
+        return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    int rc = a2t_sync(c);
+    if (rc) return rc;
+    DeviceGuard dg(c->cfg.device);
+    const StreamState& s = c->ss[stream];
+    const a2t_config& k = c->cfg;
+    const size_t elt = k.dtype == A2T_F32 ? 4 : 2;
+    const size_t row = (size_t)k.head_dim * elt;       // one head of one row
+    const size_t dpitch = row * k.n_kv_heads;          // host row pitch
+    const int T = s.kept, U = s.ring, head = s.head, cap = k.unit_rows;
+    const int first = std::min(U, cap - head), second = U - first;
+    for (int which = 0; which < 2; ++which) {
+        char* dst = static_cast<char*>(which ? vout : kout);
+        if (!dst) continue;
+        const char* kept = static_cast<const char*>(which ? c->dev.v_kept : c->dev.k_kept);
+        const char* ring = static_cast<const char*>(which ? c->dev.v_unit : c->dev.k_unit);
+        for (int g = 0; g < k.n_kv_heads; ++g) {
+            const char* kb = kept + pool_index(c->dev, layer, stream, g, k.kept_rows, 0) * elt;
+            const char* ub = ring + pool_index(c->dev, layer, stream, g, k.unit_rows, 0) * elt;
+            if (T && hipMemcpy2D(dst + g * row, dpitch, kb, row, row, T, hipMemcpyDeviceToHost) != hipSuccess)
+                return hip_fail(c);
+            if (first && hipMemcpy2D(dst + (size_t)T * dpitch + g * row, dpitch, ub + (size_t)head * row, row,
+                                     row, first, hipMemcpyDeviceToHost) != hipSuccess)
+                return hip_fail(c);
+            if (second && hipMemcpy2D(dst + (size_t)(T + first) * dpitch + g * row, dpitch, ub, row, row,
+                                      second, hipMemcpyDeviceToHost) != hipSuccess)
+                return hip_fail(c);
+        }
+    }
+    return A2T_OK;
+}
+
+int a2t_profile_enable(a2t_cache* c, const char* kernel_filter) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    c->prof_on = kernel_filter != nullptr;
+    c->prof_filter = kernel_filter ? kernel_filter : "";
+    return A2T_OK;
+}
+
+int a2t_kernel_time(a2t_cache* c, const char* kernel, int64_t* launches, double* total_ms) {
+    if (!c || !kernel) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    DeviceGuard dg(c->cfg.device);
+    prof_harvest(c, true);
+    int64_t n = 0;
+    double ms = 0;
+    for (auto it = c->prof_acc.begin(); it != c->prof_acc.end();) {
+        if (std::strstr(it->first.c_str(), kernel)) {
+            n += it->second.first;
+            ms += it->second.second;
+            it = c->prof_acc.erase(it);
+        } else {
+            ++it;
+        }
+    }
+    if (launches) *launches = n;
+    if (total_ms) *total_ms = ms;
+    return A2T_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,221 @@
+"""Test harness: drives libA2T (through its binding) and the CPU oracle on the
+same seeded inputs.  Test infrastructure; not collected by pytest."""
+from __future__ import annotations
+
+import numpy as np
+
+from synth.streams import WorkloadConfig, step_values
+
+
+def row_bounds(spec):
+    """Rows a stream can need: ring rows (all steps) and retained rows (a
+    structural upper bound: every non-evictable row of the stream)."""
+    total = spec.total_rows()
+    keep = sum(int(np.isin(st.seg, (0, 3, 4)).sum()) for st in spec.steps)
+    max_step = max(st.n for st in spec.steps)
+    return total, keep, max_step
+
+
+def torch_dtype(cfg: WorkloadConfig):
+    import torch
+    return torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+
+
+def to_gpu(x: np.ndarray, cfg: WorkloadConfig):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to("cuda").to(torch_dtype(cfg))
+
+
+def from_gpu(t) -> np.ndarray:
+    import torch
+    return t.to(torch.float32).cpu().numpy()
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+def make_cache(cfg: WorkloadConfig, n_streams: int, unit_rows: int, kept_rows: int,
+               max_step_rows: int, n_layers=None, dtype=None):
+    import paper_2609_31224_amd as a2t
+    dt = {"f32": a2t.A2T_F32, "bf16": a2t.A2T_BF16}[dtype or cfg.dtype]
+    return a2t.a2t_cache_create(n_layers or cfg.n_layers, n_streams, cfg.n_q_heads,
+                                cfg.n_kv_heads, cfg.head_dim, dt, unit_rows, kept_rows,
+                                max_step_rows, rope_theta=cfg.rope_theta,
+                                attn_scale=cfg.scale)
+
+
+def gpu_values(cfg, seed, spec, st, layers):
+    return step_values(cfg, seed, spec.stream, st.key, st.n, layers)
+
+
+class Mismatch(AssertionError):
+    pass
+
+
+def _bf16_tol(ref):
+    return np.abs(ref) * 2.0 ** -8 + 1e-6
+
+
+class Lockstep:
+    """Run streams through libA2T and the oracle together, step by step.
+
+    ``specs`` are StreamSpecs that share one cache (one stream id each, in
+    order).  Values come from the seeded generator for ``layers_checked``;
+    every other layer reuses the values of the first checked layer (its
+    outputs are computed but not compared).  Every step: per layer append +
+    attention; after the last layer, eviction.  Checked each step: attention
+    outputs on the checked layers (``tol`` max abs error), eviction counts and
+    flags, the device layout, the device eviction mask / compaction indices,
+    the stored K/V against the oracle, and that compaction moved every
+    surviving row's bytes unchanged.
+    """
+
+    def __init__(self, cfg, seed, specs, *, layers_checked, n_layers, budgets, window,
+                 unit_rows, kept_rows, max_step, tol, dtype=None, check_kv_every=1,
+                 all_layers_append=False, query_rows=None):
+        from oracle.cache import OracleCache
+        import paper_2609_31224_amd as a2t
+        self.a2t = a2t
+        self.cfg, self.seed, self.specs = cfg, seed, specs
+        self.dtype = dtype or cfg.dtype
+        self.layers_checked = list(layers_checked)
+        self.n_layers = n_layers
+        self.budgets = list(budgets)
+        self.window = window
+        self.tol = tol
+        self.check_kv_every = check_kv_every
+        self.all_layers_append = all_layers_append
+        self.query_rows = query_rows
+        self.cache = make_cache(cfg, len(specs), unit_rows, kept_rows, max_step, n_layers=n_layers,
+                                dtype=self.dtype)
+        self.oracles = [OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, self.layers_checked,
+                                    theta=cfg.rope_theta, scale=cfg.scale) for _ in specs]
+        self.max_err = 0.0
+        self.steps_done = 0
+        self.evictions = 0
+        self.unmet_steps = 0
+        self.outputs = []
+
+    def _upload(self, x):
+        import torch
+        t = torch.from_numpy(np.ascontiguousarray(x, np.float32)).to("cuda")
+        return t.to(torch.float32 if self.dtype == "f32" else torch.bfloat16)
+
+    def close(self):
+        self.a2t.a2t_cache_destroy(self.cache)
+
+    def run(self, n_global_steps=None, offsets=None):
+        offsets = offsets or [0] * len(self.specs)
+        T = max(o + len(s.steps) for o, s in zip(offsets, self.specs))
+        if n_global_steps is not None:
+            T = min(T, n_global_steps)
+        for t in range(T):
+            act = [(i, s.steps[t - o]) for i, (o, s) in enumerate(zip(offsets, self.specs))
+                   if 0 <= t - o < len(s.steps)]
+            if act:
+                self.step(act, t)
+        return self
+
+    def step(self, act, t):
+        a2t, cfg = self.a2t, self.cfg
+        import torch
+        ids = [i for i, _ in act]
+        n = [st.n for _, st in act]
+        nq = [min(st.n, self.query_rows) if self.query_rows else st.n for _, st in act]
+        decode = all(st.decode for _, st in act)
+        vals = [step_values(cfg, self.seed, self.specs[i].stream, st.key, st.n, self.layers_checked)
+                for i, st in act]
+        seg = np.concatenate([st.seg for _, st in act])
+        pos = np.concatenate([st.pos for _, st in act])
+        unit = [st.unit for _, st in act]
+        for (i, st), vv in zip(act, vals):
+            k = {l: vv["k"][j] for j, l in enumerate(self.layers_checked)}
+            v = {l: vv["v"][j] for j, l in enumerate(self.layers_checked)}
+            self.oracles[i].append(st.seg, st.pos, st.unit, k, v)
+
+        def packed(name, layer):
+            j = self.layers_checked.index(layer) if layer in self.layers_checked else 0
+            return np.concatenate([vv[name][j] for vv in vals])
+
+        if self.all_layers_append:
+            kk = self._upload(np.stack([packed("k", l) for l in range(self.n_layers)]))
+            vv_ = self._upload(np.stack([packed("v", l) for l in range(self.n_layers)]))
+            a2t.a2t_append(self.cache, a2t.A2T_ALL_LAYERS, ids, n, kk, vv_, seg, pos, unit)
+        for layer in range(self.n_layers):
+            if not self.all_layers_append:
+                kk, vv_ = self._upload(packed("k", layer)), self._upload(packed("v", layer))
+                meta = (seg, pos, unit) if layer == 0 else (None, None, None)
+                a2t.a2t_append(self.cache, layer, ids, n, kk, vv_, *meta)
+            qfull = packed("q", layer)
+            # queries: the last nq rows of every stream's step
+            rows, off = [], 0
+            for a, b in zip(n, nq):
+                rows.extend(range(off + a - b, off + a))
+                off += a
+            q = self._upload(qfull[rows])
+            o = torch.empty_like(q)
+            if decode:
+                a2t.a2t_decode_attn(self.cache, layer, ids, q, o)
+            else:
+                a2t.a2t_chunk_attn(self.cache, layer, ids, nq, q, o)
+            if layer in self.layers_checked:
+                og = o.to(torch.float32).cpu().numpy()
+                off = 0
+                for (i, st), b in zip(act, nq):
+                    want = self.oracles[i].attention(layer, qfull[rows][off:off + b], b)
+                    err = float(np.abs(og[off:off + b] - want).max())
+                    self.max_err = max(self.max_err, err)
+                    if not err <= self.tol:
+                        raise Mismatch(f"step {t} stream {i} layer {layer}: attention max err {err}")
+                    self.outputs.append(og[off:off + b].copy())
+                    off += b
+
+        check_kv = (self.steps_done % self.check_kv_every) == 0
+        pre_kv = {}
+        if check_kv:
+            for i, _ in act:
+                for l in self.layers_checked[:1]:
+                    pre_kv[(i, l)] = a2t.a2t_read_kv(self.cache, l, i)
+                    self._check_kv(i, l, *pre_kv[(i, l)], t)
+        budgets = [self.budgets[i] for i in ids]
+        n_ev, unmet = a2t.a2t_evict(self.cache, ids, budgets, self.window)
+        for j, (i, st) in enumerate(act):
+            rec = self.oracles[i].evict(self.budgets[i], self.window)
+            if int(n_ev[j]) != rec.n_evicted or bool(unmet[j]) != rec.plan.budget_unmet:
+                raise Mismatch(f"step {t} stream {i}: evicted {n_ev[j]}/{rec.n_evicted} "
+                               f"unmet {unmet[j]}/{rec.plan.budget_unmet}")
+            self.unmet_steps += int(rec.plan.budget_unmet)
+            p, s, u = a2t.a2t_read_layout(self.cache, i)
+            if not (np.array_equal(p, rec.pos) and np.array_equal(s, rec.seg)
+                    and np.array_equal(u, rec.unit)):
+                raise Mismatch(f"step {t} stream {i}: layout differs")
+            if rec.n_evicted:
+                self.evictions += 1
+                n_pre, mask, slot = a2t.a2t_read_last_evict(self.cache, i)
+                if n_pre != rec.plan.n_pre or not np.array_equal(mask.astype(bool), rec.plan.evict_mask) \
+                        or not np.array_equal(slot, rec.new_slot):
+                    raise Mismatch(f"step {t} stream {i}: eviction mask / new_slot differ")
+                if (i, self.layers_checked[0]) in pre_kv:
+                    k0, v0 = pre_kv[(i, self.layers_checked[0])]
+                    k1, v1 = a2t.a2t_read_kv(self.cache, self.layers_checked[0], i)
+                    keep = slot >= 0
+                    if not (np.array_equal(k1[slot[keep]], k0[keep]) and
+                            np.array_equal(v1[slot[keep]], v0[keep])):
+                        raise Mismatch(f"step {t} stream {i}: compaction changed row bytes")
+        self.steps_done += 1
+
+    def _check_kv(self, i, layer, k, v, t):
+        o = self.oracles[i]
+        if self.dtype == "f32":
+            kf, vf = k, v
+            ktol = 1e-5
+            vtol = 0.0
+        else:
+            kf, vf = bf16_bits_to_f32(k), bf16_bits_to_f32(v)
+            ktol = _bf16_tol(o.k[layer])
+            vtol = 0.0
+        if kf.shape != o.k[layer].shape or not np.all(np.abs(kf - o.k[layer]) <= ktol):
+            raise Mismatch(f"step {t} stream {i} layer {layer}: stored K differs from the oracle")
+        if not np.all(np.abs(vf - o.v[layer]) <= vtol):
+            raise Mismatch(f"step {t} stream {i} layer {layer}: stored V differs")

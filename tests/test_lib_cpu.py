@@ -1,0 +1,212 @@
+"""CPU tests of libA2T: the library loads and exports every call the header
+declares; argument validation and the host-side eviction planner (a cache
+created with A2T_FLAG_HOST_ONLY runs no device work) match the oracle's
+policy decisions bit for bit."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2609_31224_amd as a2t
+from oracle.replay import replay_metadata
+from synth.streams import CONFIGS, make_workload, tiny_stream
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "a2t.h")
+
+
+def header_calls():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(a2t_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_call_is_exported():
+    calls = header_calls()
+    assert len(calls) >= 16
+    lib = ctypes.CDLL(a2t.LIB_PATH)
+    for name in calls:
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", a2t.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    exported = set(re.findall(r" T (a2t_\w+)", out))
+    assert set(calls) <= exported
+    assert set(a2t.EXPORTED) == set(calls)
+
+
+def test_abi_version_and_status_strings():
+    assert a2t.a2t_abi_version() == 1
+    assert a2t.a2t_status_str(0) == "ok"
+    for s in range(-7, 0):
+        assert a2t.a2t_status_str(s) != "unknown status"
+
+
+def test_device_cache_without_gpu_fails_loudly():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is visible")
+    with pytest.raises(a2t.A2TError) as e:
+        a2t.a2t_cache_create(1, 1, 4, 1, 64, a2t.A2T_F32, 64, 64, 32)
+    assert e.value.status == a2t.A2T_ERR_NODEV
+
+
+def host_cache(n_streams=1, unit_rows=4096, kept_rows=4096, max_step=128, layers=2, Hq=4, Hkv=1, D=64):
+    return a2t.a2t_cache_create(layers, n_streams, Hq, Hkv, D, a2t.A2T_F32, unit_rows,
+                                kept_rows, max_step, flags=a2t.A2T_FLAG_HOST_ONLY)
+
+
+def append_all(c, sid, st):
+    a2t.a2t_append(c, a2t.A2T_ALL_LAYERS, [sid], [st.n], None, None, st.seg, st.pos, [st.unit])
+
+
+def test_create_validation():
+    bad = [
+        dict(n_q_heads=6, n_kv_heads=4),       # not a multiple
+        dict(n_q_heads=48, n_kv_heads=4),      # group of 12
+        dict(head_dim=96),
+        dict(max_step_rows=2000),
+        dict(unit_rows=0),
+    ]
+    base = dict(n_layers=1, n_streams=1, n_q_heads=4, n_kv_heads=1, head_dim=64,
+                dtype=a2t.A2T_F32, unit_rows=64, kept_rows=64, max_step_rows=16,
+                flags=a2t.A2T_FLAG_HOST_ONLY)
+    for b in bad:
+        kw = dict(base, **b)
+        with pytest.raises(a2t.A2TError) as e:
+            a2t.a2t_cache_create(**kw)
+        assert e.value.status == a2t.A2T_ERR_INVALID
+
+
+def _status(fn, *a):
+    try:
+        fn(*a)
+        return 0
+    except a2t.A2TError as e:
+        return e.status
+
+
+def test_append_errors_leave_state_unchanged():
+    c = host_cache(n_streams=2, unit_rows=32, kept_rows=8, max_step=32, layers=2)
+    ok = a2t.a2t_append(c, 0, [0], [3], None, None, [1, 1, 3], [0, 1, 2], [0])
+    before = a2t.a2t_stream_info_get(c, 0)
+    cases = [
+        (a2t.A2T_ERR_STATE, (c, 0, [0], [2], None, None, [1, 1], [3, 4], [1])),   # layer 1 missing
+        (a2t.A2T_ERR_STATE, (c, 1, [1], [2], None, None, None, None, None)),      # no open step
+        (a2t.A2T_ERR_POS, (c, 1, [0], [2], None, None, None, None, None)),        # row count differs
+        (a2t.A2T_ERR_POS, (c, 1, [0], [3], None, None, [1, 1, 2], None, None)),   # seg differs
+        (a2t.A2T_ERR_INVALID, (c, 2, [0], [3], None, None, None, None, None)),    # layer out of range
+        (a2t.A2T_ERR_INVALID, (c, 1, [0, 0], [3, 3], None, None, None, None, None)),  # duplicate id
+        (a2t.A2T_ERR_INVALID, (c, 1, [5], [3], None, None, None, None, None)),    # bad stream
+    ]
+    for want, args in cases:
+        assert _status(a2t.a2t_append, *args) == want, args
+        assert a2t.a2t_stream_info_get(c, 0) == before
+    assert _status(a2t.a2t_append, c, 1, [0], [3], None, None, None, None, None) == 0
+    # next step: ordering errors
+    cases = [
+        (a2t.A2T_ERR_POS, (c, 0, [0], [2], None, None, [1, 1], [2, 5], [1])),     # pos not increasing
+        (a2t.A2T_ERR_POS, (c, 0, [0], [2], None, None, [1, 1], [5, 5], [1])),     # repeated pos
+        (a2t.A2T_ERR_INVALID, (c, 0, [0], [2], None, None, [1, 7], [5, 6], [1])),  # bad class
+        (a2t.A2T_ERR_INVALID, (c, 0, [0], [2], None, None, [0, 0], [5, 6], [1])),  # prefix in a unit
+        (a2t.A2T_ERR_POS, (c, 0, [0], [1], None, None, [0], [5], [-1])),          # prefix after units
+        (a2t.A2T_ERR_INVALID, (c, 0, [0], [0], None, None, [], [], [1])),          # empty step
+        (a2t.A2T_ERR_INVALID, (c, 0, [0], [40], None, None, [1] * 40, list(range(5, 45)), [1])),  # > max_step
+        (a2t.A2T_ERR_CAPACITY, (c, 0, [0], [30], None, None, [1] * 30, list(range(5, 35)), [1])),  # ring full
+    ]
+    before = a2t.a2t_stream_info_get(c, 0)
+    for want, args in cases:
+        assert _status(a2t.a2t_append, *args) == want, args
+        assert a2t.a2t_stream_info_get(c, 0) == before
+    # attention on a host-only cache is refused
+    assert _status(a2t.a2t_chunk_attn, c, 0, [0], [1], 16, 32) == a2t.A2T_ERR_NODEV
+    assert _status(a2t.a2t_chunk_attn, c, 0, [0], [1], 0, 32) == a2t.A2T_ERR_INVALID
+    assert _status(a2t.a2t_chunk_attn, c, 0, [0], [4], 16, 32) == a2t.A2T_ERR_STATE  # > step rows
+    a2t.a2t_cache_destroy(c)
+
+
+def test_evict_errors():
+    c = host_cache(unit_rows=64, kept_rows=1, layers=1)
+    a2t.a2t_append(c, 0, [0], [3], None, None, [1, 3, 3], [0, 1, 2], [0])
+    a2t.a2t_append(c, 0, [0], [3], None, None, [1, 3, 3], [3, 4, 5], [1])
+    assert _status(a2t.a2t_evict, c, [0], [-1], 0) == a2t.A2T_ERR_INVALID
+    assert _status(a2t.a2t_evict, c, [0], [0], -1) == a2t.A2T_ERR_INVALID
+    before = a2t.a2t_stream_info_get(c, 0)
+    # evicting unit 0 would retain 2 text rows: the kept region holds 1
+    assert _status(a2t.a2t_evict, c, [0], [4], 1) == a2t.A2T_ERR_CAPACITY
+    assert a2t.a2t_stream_info_get(c, 0) == before
+    c2 = host_cache(layers=2)
+    a2t.a2t_append(c2, 0, [0], [1], None, None, [1], [0], [0])
+    assert _status(a2t.a2t_evict, c2, [0], [0], 0) == a2t.A2T_ERR_STATE   # layer 1 not appended
+
+
+def _library_trace(spec, budget, window, unit_rows, kept_rows, max_step):
+    c = host_cache(unit_rows=unit_rows, kept_rows=kept_rows, max_step=max_step, layers=1)
+    rows = []
+    for st in spec.steps:
+        append_all(c, 0, st)
+        pre = a2t.a2t_stream_info_get(c, 0)["resident"]
+        n_ev, unmet = a2t.a2t_evict(c, [0], [budget], window)
+        info = a2t.a2t_stream_info_get(c, 0)
+        rows.append((pre, int(n_ev[0]), bool(unmet[0]), info["resident"], info["last_evicted_unit"]))
+    peak = a2t.a2t_stream_info_get(c, 0)["peak"]
+    a2t.a2t_cache_destroy(c)
+    return rows, peak
+
+
+def _compare(spec, budget, window):
+    total = spec.total_rows()
+    rows, peak = _library_trace(spec, budget, window, total + 1, total + 1,
+                                max(st.n for st in spec.steps))
+    tr = replay_metadata(spec, budget, window)
+    for (pre, n_ev, unmet, post, last_u), t in zip(rows, tr.steps):
+        assert pre == t.n_pre
+        assert n_ev == t.n_pre - t.n_post
+        assert unmet == t.budget_unmet
+        assert post == t.n_post
+        if t.units:
+            assert last_u == t.units[-1]
+    assert peak == tr.peak
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_planner_matches_oracle_config0(seed):
+    cfg = CONFIGS[0]
+    _compare(make_workload(cfg, seed=seed).streams[0], cfg.budget, cfg.window)
+
+
+def test_planner_matches_oracle_config1():
+    cfg = CONFIGS[1]
+    _compare(make_workload(cfg).streams[0], cfg.budget, cfg.window)
+
+
+def test_planner_matches_oracle_config2_streams():
+    w = make_workload(2)
+    for spec in w.streams[:6]:
+        _compare(spec, spec.budget, w.config.window)
+
+
+def test_planner_matches_oracle_config3_fill_and_decode():
+    w = make_workload(3, n_streams=2)
+    for spec in w.streams:
+        _compare(spec, spec.budget, w.config.window)
+
+
+@pytest.mark.slow
+def test_planner_matches_oracle_config4_stream():
+    w = make_workload(4, n_streams=1)
+    _compare(w.streams[0], w.config.budget, w.config.window)
+
+
+def test_planner_golden_and_edge_streams():
+    # prefix, decode rows, W = 0 and B = 0 on hand-shaped streams
+    shapes = [
+        ([[1, 1, 2, 3, 2]] * 6, 10, 1, 2),
+        ([[1, 1, 3]] * 8, 0, 2, 0),
+        ([[1, 1, 2, 2], [4], [1, 1, 3], [4], [4]], 6, 1, 0),
+        ([[1, 3]] * 5, 3, 0, 0),
+        ([[3, 3], [1, 1], [3], [1, 2, 2, 1]] * 3, 4, 1, 3),
+    ]
+    for units, B, W, prefix in shapes:
+        _compare(tiny_stream(units, prefix=prefix, pos_gap=2), B, W)
