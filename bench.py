@@ -194,6 +194,7 @@ def main():
     for j in range(args.steps):
         run_unit(args.warmup + j, record=True)
         evs[j + 1].record(stream)
+    t_enqueue = time.perf_counter() - t_wall
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     unit_ms = np.array([evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps)])
@@ -224,8 +225,8 @@ def main():
         kern[name] = {"launches": n_launch, "avg_us": (ms * 1e3 / n_launch) if n_launch else None}
     a2t.a2t_profile_enable(cache, None)
     prof_attn_bytes = np.mean([attn_bytes(R, n, cfg) for (R, n, _, _) in R_log]) if R_log else 0.0
-    attn_us = kern["attn_mfma"]["avg_us"] or float("nan")
-    achieved = prof_attn_bytes / (attn_us * 1e-6) / 1e9
+    attn_us = kern["attn_mfma"]["avg_us"]
+    achieved = prof_attn_bytes / (attn_us * 1e-6) / 1e9 if attn_us else None
 
     lib.a2t_stream_info_get(h, 0, C.byref(info))
     peak = info.peak
@@ -265,7 +266,7 @@ def main():
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
+            "frac": achieved / HBM_PEAK_GBPS if achieved else None,
             "traffic": None,
             "avg_launch_us": attn_us,
             "alg_bytes_per_launch": prof_attn_bytes,
@@ -280,6 +281,7 @@ def main():
         "rows_without_eviction": rows_no_evict,
         "peak_reduction": 1.0 - peak / rows_no_evict,
         "host_wall_s": t_wall,
+        "host_enqueue_ms_per_step": t_enqueue * 1e3 / args.steps,
         "cpu_baseline": base_line,
     }
     print(json.dumps(result), flush=True)

@@ -63,6 +63,14 @@ class a2t_stream_info(C.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_31224_amd.build`")
+    # torch ships its own HIP runtime and loads it under the unversioned name.
+    # Loading torch first lets libA2T's libamdhip64.so.7 dependency resolve,
+    # by SONAME, to that same runtime: one HIP/HSA runtime per process, so
+    # torch's device pointers and streams are valid in libA2T.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = C.CDLL(LIB_PATH)
     P, I32, VP = C.POINTER, C.c_int32, C.c_void_p
     sig = {

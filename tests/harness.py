@@ -4,7 +4,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from synth.streams import WorkloadConfig, step_values
+from synth.streams import WorkloadConfig, bf16_round, step_values
 
 
 def row_bounds(spec):
@@ -126,6 +126,9 @@ class Lockstep:
         decode = all(st.decode for _, st in act)
         vals = [step_values(cfg, self.seed, self.specs[i].stream, st.key, st.n, self.layers_checked)
                 for i, st in act]
+        if self.dtype == "bf16" and cfg.dtype != "bf16":
+            # a bf16 run of an fp32 workload: both sides see the bf16-rounded inputs
+            vals = [{k_: bf16_round(a) for k_, a in vv.items()} for vv in vals]
         seg = np.concatenate([st.seg for _, st in act])
         pos = np.concatenate([st.pos for _, st in act])
         unit = [st.unit for _, st in act]
@@ -215,7 +218,14 @@ class Lockstep:
             kf, vf = bf16_bits_to_f32(k), bf16_bits_to_f32(v)
             ktol = _bf16_tol(o.k[layer])
             vtol = 0.0
-        if kf.shape != o.k[layer].shape or not np.all(np.abs(kf - o.k[layer]) <= ktol):
-            raise Mismatch(f"step {t} stream {i} layer {layer}: stored K differs from the oracle")
+        if kf.shape != o.k[layer].shape:
+            raise Mismatch(f"step {t} stream {i} layer {layer}: stored K shape {kf.shape} "
+                           f"vs {o.k[layer].shape}")
+        bad = np.abs(kf - o.k[layer]) > ktol
+        if bad.any():
+            idx = tuple(int(x) for x in np.argwhere(bad)[0])
+            raise Mismatch(f"step {t} stream {i} layer {layer}: stored K differs from the oracle "
+                           f"at {bad.sum()} elements, first {idx}: {kf[idx]} vs {o.k[layer][idx]}; "
+                           f"rows {sorted(set(int(r) for r in np.argwhere(bad)[:, 0]))[:20]}")
         if not np.all(np.abs(vf - o.v[layer]) <= vtol):
             raise Mismatch(f"step {t} stream {i} layer {layer}: stored V differs")
