@@ -99,6 +99,8 @@ def main():
     ap.add_argument("--cpu-sample-layers", type=int, default=4)
     ap.add_argument("--profile-steps", type=int, default=100,
                     help="extra timed units with per-kernel HIP events (roofline)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="per layer a2t_append then a2t_chunk_attn (default: a2t_append_attn)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -160,16 +162,19 @@ def main():
         for layer in range(L):
             off_q = (p * L + layer) * row_stride_q
             off_kv = (p * L + layer) * row_stride_kv
-            if layer == 0:
-                rc = lib.a2t_append(h, 0, 1, ids, nrows, k_base + off_kv, v_base + off_kv, seg, pos, unit)
+            meta = (seg, pos, unit) if layer == 0 else (None, None, None)
+            if args.unfused:
+                rc = lib.a2t_append(h, layer, 1, ids, nrows, k_base + off_kv, v_base + off_kv, *meta)
+                if rc:
+                    raise a2t.A2TError(rc, "a2t_append")
+                rc = lib.a2t_chunk_attn(h, layer, 1, ids, nrows, q_base + off_q, o_ptr)
+                if rc:
+                    raise a2t.A2TError(rc, "a2t_chunk_attn")
             else:
-                rc = lib.a2t_append(h, layer, 1, ids, nrows, k_base + off_kv, v_base + off_kv,
-                                    None, None, None)
-            if rc:
-                raise a2t.A2TError(rc, "a2t_append")
-            rc = lib.a2t_chunk_attn(h, layer, 1, ids, nrows, q_base + off_q, o_ptr)
-            if rc:
-                raise a2t.A2TError(rc, "a2t_chunk_attn")
+                rc = lib.a2t_append_attn(h, layer, 1, ids, nrows, k_base + off_kv, v_base + off_kv,
+                                         *meta, nrows, q_base + off_q, o_ptr)
+                if rc:
+                    raise a2t.A2TError(rc, "a2t_append_attn")
         if record:
             lib.a2t_stream_info_get(h, 0, C.byref(info))
             R_attn = info.resident
@@ -258,6 +263,8 @@ def main():
                         "bf16, units of 17 acoustic + 2 delimiter + Poisson(3) transcript rows, "
                         "budget 4096 rows, recent window 30 units",
             "timed_units": [args.warmup, args.warmup + args.steps],
+            "calls": "a2t_append + a2t_chunk_attn per layer" if args.unfused
+                     else "a2t_append_attn per layer",
             "seed": args.seed,
         },
         "roofline": {

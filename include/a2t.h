@@ -189,6 +189,17 @@ int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* st
 int a2t_chunk_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* stream_ids,
                    const int32_t* n_q, const void* q, void* o);
 
+/* a2t_append on one layer followed by a2t_chunk_attn on that layer, in one
+ * launch where the kernels allow it (bf16 caches): the workgroups whose key
+ * tiles hold the step's new rows rotate and store them while staging them
+ * for attention.  Arguments as in the two calls (layer 0..L-1 only; n_q
+ * host [n_streams] with 1 <= n_q <= n_rows; q and o packed [sum n_q][Hq][D]).
+ * Results and cache contents are the same as the two calls. */
+int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* stream_ids,
+                    const int32_t* n_rows, const void* k, const void* v, const uint8_t* seg,
+                    const int32_t* pos, const int32_t* unit_id, const int32_t* n_q,
+                    const void* q, void* o);
+
 /* Decode attention while speaking: one query per stream, the stream's newest
  * row (Sec. 3.1: response tokens are decoded one by one over the cache).
  *   q, o  device [n_streams][Hq][D].  Errors as a2t_chunk_attn. */

@@ -35,7 +35,7 @@ SEG_PREFIX, SEG_ACOUSTIC, SEG_DELIM, SEG_TEXT, SEG_RESPONSE = 0, 1, 2, 3, 4
 
 EXPORTED = (
     "a2t_cache_create", "a2t_cache_destroy", "a2t_set_stream", "a2t_append",
-    "a2t_chunk_attn", "a2t_decode_attn", "a2t_evict", "a2t_stream_info_get",
+    "a2t_chunk_attn", "a2t_append_attn", "a2t_decode_attn", "a2t_evict", "a2t_stream_info_get",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
     "a2t_profile_enable", "a2t_kernel_time", "a2t_status_str", "a2t_abi_version",
 )
@@ -62,7 +62,7 @@ class a2t_stream_info(C.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_31224_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_31224_amd/build.py`")
     # torch ships its own HIP runtime and loads it under the unversioned name.
     # Loading torch first lets libA2T's libamdhip64.so.7 dependency resolve,
     # by SONAME, to that same runtime: one HIP/HSA runtime per process, so
@@ -79,6 +79,8 @@ def _load():
         "a2t_set_stream": (C.c_int, [VP, VP]),
         "a2t_append": (C.c_int, [VP, I32, I32, P(I32), P(I32), VP, VP, P(C.c_uint8), P(I32), P(I32)]),
         "a2t_chunk_attn": (C.c_int, [VP, I32, I32, P(I32), P(I32), VP, VP]),
+        "a2t_append_attn": (C.c_int, [VP, I32, I32, P(I32), P(I32), VP, VP, P(C.c_uint8), P(I32),
+                                      P(I32), P(I32), VP, VP]),
         "a2t_decode_attn": (C.c_int, [VP, I32, I32, P(I32), VP, VP]),
         "a2t_evict": (C.c_int, [VP, I32, P(I32), P(I32), I32, P(I32), P(C.c_uint8)]),
         "a2t_stream_info_get": (C.c_int, [VP, I32, P(a2t_stream_info)]),
@@ -217,6 +219,22 @@ def a2t_chunk_attn(c: Cache, layer: int, stream_ids: Sequence[int], n_q: Sequenc
     rc = _lib.a2t_chunk_attn(c.ptr, layer, len(ids), _p(ids, C.c_int32), _p(nq, C.c_int32),
                              _dev(q, "q", dt), _dev(o, "o", dt))
     _check(rc, "a2t_chunk_attn")
+
+
+def a2t_append_attn(c: Cache, layer: int, stream_ids: Sequence[int], n_rows: Sequence[int], k, v,
+                    seg, pos, unit_id, n_q: Sequence[int], q, o) -> None:
+    ids, nr, nq = _i32(stream_ids), _i32(n_rows), _i32(n_q)
+    if not (ids.shape == nr.shape == nq.shape):
+        raise ValueError("stream_ids, n_rows and n_q differ in length")
+    sg = None if seg is None else _u8(seg)
+    ps = None if pos is None else _i32(pos)
+    un = None if unit_id is None else _i32(unit_id)
+    dt = c.torch_dtype if not isinstance(k, (int, type(None))) else None
+    rc = _lib.a2t_append_attn(c.ptr, layer, len(ids), _p(ids, C.c_int32), _p(nr, C.c_int32),
+                              _dev(k, "k", dt), _dev(v, "v", dt), _p(sg, C.c_uint8),
+                              _p(ps, C.c_int32), _p(un, C.c_int32), _p(nq, C.c_int32),
+                              _dev(q, "q", dt), _dev(o, "o", dt))
+    _check(rc, "a2t_append_attn")
 
 
 def a2t_decode_attn(c: Cache, layer: int, stream_ids: Sequence[int], q, o) -> None:

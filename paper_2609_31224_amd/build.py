@@ -1,7 +1,8 @@
 """Build libA2T.so in-tree with hipcc for gfx950.
 
-Usage: ``python -m paper_2609_31224_amd.build`` (or ``build()`` from Python).
-The library lands next to this file; a build always recompiles.
+Usage: ``python paper_2609_31224_amd/build.py`` (run it as a script: importing
+the package itself loads the library).  The library lands next to this file;
+a build always recompiles.
 """
 from __future__ import annotations
 

@@ -83,6 +83,10 @@ struct a2t_cache {
     int next_slot = 0;
     std::vector<hipEvent_t> slot_ev;
     std::vector<uint8_t> slot_live;
+    // per-call scratch, sized at creation (no allocation on the hot path)
+    std::vector<uint32_t> seen;      // stream id -> call stamp
+    uint32_t stamp = 0;
+    std::vector<int32_t> tmp_nq, tmp_row0, tmp_in0;
     // attention tuning
     int target_wgs = 1024;
     int force_splits = 0;
@@ -189,12 +193,16 @@ bool stage_release(a2t_cache* c, int slot) {
     return true;
 }
 
-int check_streams(const a2t_cache* c, int32_t n, const int32_t* ids) {
+int check_streams(a2t_cache* c, int32_t n, const int32_t* ids) {
     if (n < 1 || n > c->cfg.n_streams || !ids) return A2T_ERR_INVALID;
-    std::vector<uint8_t> seen(c->cfg.n_streams, 0);
+    if (++c->stamp == 0) {  // wrapped: clear the stamps
+        std::fill(c->seen.begin(), c->seen.end(), 0u);
+        c->stamp = 1;
+    }
     for (int i = 0; i < n; ++i) {
-        if (ids[i] < 0 || ids[i] >= c->cfg.n_streams || seen[ids[i]]) return A2T_ERR_INVALID;
-        seen[ids[i]] = 1;
+        if (ids[i] < 0 || ids[i] >= c->cfg.n_streams || c->seen[ids[i]] == c->stamp)
+            return A2T_ERR_INVALID;
+        c->seen[ids[i]] = c->stamp;
     }
     return A2T_OK;
 }
@@ -213,7 +221,7 @@ int choose_splits(const a2t_cache* c, int n_desc, int max_R, int64_t floats_per_
         // keep at least two tiles per split unless forced
         sp = std::min(sp, std::max(1, n_tiles / 2));
     }
-    sp = std::min(sp, n_tiles);
+    sp = std::min(std::min(sp, n_tiles), kMaxSplits);
     if (sp > 1) {
         const int64_t cap = c->dev.ws_floats / std::max<int64_t>(1, floats_per_split_all);
         sp = (int)std::min<int64_t>(sp, std::max<int64_t>(1, cap));
@@ -222,8 +230,12 @@ int choose_splits(const a2t_cache* c, int n_desc, int max_R, int64_t floats_per_
 }
 
 // One attention launch (plus merge) over up to kMaxDesc streams.
+// With in_row0 non-null (bf16 MFMA path only) the launch also appends each
+// stream's open-step rows of `layer` from k_in / v_in.
 int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_t* n_q,
-                const int32_t* q_row0, const void* q, void* o, bool decode) {
+                const int32_t* q_row0, const void* q, void* o, bool decode,
+                const int32_t* in_row0 = nullptr, const void* k_in = nullptr,
+                const void* v_in = nullptr) {
     AttnBatch b{};
     b.count = n;
     b.layer = layer;
@@ -250,6 +262,8 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         d.rope_row0 = s.step_rows - n_q[i];
         const int n_tiles = (d.R + kTileKeys - 1) / kTileKeys;
         d.splits = std::max(1, std::min(splits, n_tiles));
+        d.n_new = in_row0 ? s.step_rows : 0;
+        d.in_row0 = in_row0 ? in_row0[i] : 0;
         d.ws_off = off;
         if (d.splits > 1) off += (int64_t)d.splits * c->cfg.n_kv_heads * G * d.n_q * (c->cfg.head_dim + 2);
     }
@@ -260,7 +274,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     {
         ProfScope ps(c, valu ? "attn_valu" : "attn_mfma");
         e = valu ? launch_attn_valu(c->dev, b, q, o, c->stream)
-                 : launch_attn_mfma(c->dev, b, q, o, c->stream);
+                 : launch_attn_mfma(c->dev, b, q, o, k_in, v_in, c->stream);
     }
     if (e != hipSuccess) return hip_fail(c);
     if (splits > 1) {
@@ -278,7 +292,8 @@ int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* i
     int rc = check_streams(c, n_streams, ids);
     if (rc) return rc;
     if (!q || !o || (!decode && !n_q)) return A2T_ERR_INVALID;
-    std::vector<int32_t> nq(n_streams), row0(n_streams);
+    std::vector<int32_t>& nq = c->tmp_nq;
+    std::vector<int32_t>& row0 = c->tmp_row0;
     int32_t acc = 0;
     for (int i = 0; i < n_streams; ++i) {
         const StreamState& s = c->ss[ids[i]];
@@ -359,7 +374,11 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     c->stream = static_cast<hipStream_t>(hip_stream);
     c->ss.resize(k.n_streams);
     for (auto& s : c->ss) s.appended.assign(k.n_layers, 1);
-    c->target_wgs = std::max(1, env_int("A2T_TARGET_WGS", 1024));
+    c->seen.assign(k.n_streams, 0u);
+    c->tmp_nq.assign(k.n_streams, 0);
+    c->tmp_row0.assign(k.n_streams, 0);
+    c->tmp_in0.assign(k.n_streams, 0);
+    c->target_wgs = std::max(1, env_int("A2T_TARGET_WGS", 256));
     c->force_splits = std::max(0, env_int("A2T_SPLITS", 0));
     c->force_valu = env_flag("A2T_FORCE_VALU");
 
@@ -459,9 +478,12 @@ int a2t_set_stream(a2t_cache* c, void* hip_stream) {
     return A2T_OK;
 }
 
-int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
-               const int32_t* n_rows, const void* kin, const void* vin, const uint8_t* seg,
-               const int32_t* pos, const int32_t* unit_id) {
+// a2t_append; with launch_rows false the rows' K/V are left for a fused
+// attention launch to store (metadata and the rotary table are still written).
+static int append_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                       const int32_t* n_rows, const void* kin, const void* vin,
+                       const uint8_t* seg, const int32_t* pos, const int32_t* unit_id,
+                       bool launch_rows) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
     const a2t_config& k = c->cfg;
@@ -566,8 +588,10 @@ int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* id
             std::memcpy(spos, pos + row, rows_here * 4);
             std::memcpy(sseg, seg + row, rows_here);
             int64_t r0 = 0;
+            sb.max_n = 0;
             for (int i = 0; i < n; ++i) {
                 const StreamState& s = c->ss[ids[i0 + i]];
+                sb.max_n = std::max(sb.max_n, n_rows[i0 + i]);
                 sb.d[i] = StepDesc{ids[i0 + i], n_rows[i0 + i], s.step_slot0, (int32_t)r0};
                 suid[i] = unit_id[i0 + i];
                 r0 += n_rows[i0 + i];
@@ -586,7 +610,7 @@ int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* id
         }
     }
     // 2. rotate and store K, store V
-    {
+    if (launch_rows) {
         int64_t in_row = 0;
         for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
             const int n = std::min(kMaxDesc, n_streams - i0);
@@ -614,9 +638,50 @@ int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* id
     return A2T_OK;
 }
 
+int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+               const int32_t* n_rows, const void* kin, const void* vin, const uint8_t* seg,
+               const int32_t* pos, const int32_t* unit_id) {
+    return append_impl(c, layer, n_streams, ids, n_rows, kin, vin, seg, pos, unit_id, true);
+}
+
 int a2t_chunk_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
                    const int32_t* n_q, const void* q, void* o) {
     return attn_common(c, layer, n_streams, ids, n_q, q, o, false);
+}
+
+int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                    const int32_t* n_rows, const void* kin, const void* vin, const uint8_t* seg,
+                    const int32_t* pos, const int32_t* unit_id, const int32_t* n_q,
+                    const void* q, void* o) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
+    if (!n_rows || !n_q || !q || !o || n_streams < 1 || n_streams > c->cfg.n_streams)
+        return A2T_ERR_INVALID;
+    for (int i = 0; i < n_streams; ++i)
+        if (n_q[i] < 1 || n_q[i] > n_rows[i]) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    const bool fused = c->cfg.dtype == A2T_BF16 && !c->force_valu;
+    int rc = append_impl(c, layer, n_streams, ids, n_rows, kin, vin, seg, pos, unit_id, !fused);
+    if (rc) return rc;
+    if (!fused) return attn_common(c, layer, n_streams, ids, n_q, q, o, false);
+    DeviceGuard dg(c->cfg.device);
+    std::vector<int32_t>& row0 = c->tmp_row0;
+    std::vector<int32_t>& in0 = c->tmp_in0;
+    int32_t acc = 0, acc_in = 0;
+    for (int i = 0; i < n_streams; ++i) {
+        row0[i] = acc;
+        in0[i] = acc_in;
+        acc += n_q[i];
+        acc_in += n_rows[i];
+    }
+    for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
+        const int n = std::min(kMaxDesc, n_streams - i0);
+        rc = attn_launch(c, layer, n, ids + i0, n_q + i0, row0.data() + i0, q, o, false,
+                         in0.data() + i0, kin, vin);
+        if (rc) return rc;
+    }
+    return A2T_OK;
 }
 
 int a2t_decode_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,

@@ -3,7 +3,11 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
+#include <string.h>
+
+#include <cstring>
 
 namespace a2t {
 
@@ -12,6 +16,8 @@ namespace a2t {
 constexpr int kMaxDesc = 64;
 // Keys per attention tile (rows staged per LDS tile).
 constexpr int kTileKeys = 64;
+// Most key splits of one attention launch (the merge stages them in LDS).
+constexpr int kMaxSplits = 128;
 
 // Device-side buffers of a cache and its shape.
 struct DevState {
@@ -48,10 +54,13 @@ struct StepDesc {
     int32_t slot0;    // ring slot of the first row
     int32_t row0;     // offset of the stream's rows in the staged arrays
 };
-struct StepBatch {
+template <int N>
+struct StepBatchT {
     int32_t count;
-    StepDesc d[kMaxDesc];
+    int32_t max_n;
+    StepDesc d[N];
 };
+using StepBatch = StepBatchT<kMaxDesc>;
 
 // ---- append
 struct AppendDesc {
@@ -60,13 +69,15 @@ struct AppendDesc {
     int32_t slot0;    // ring slot of the first row
     int32_t in_row0;  // first row in the packed k/v input
 };
-struct AppendBatch {
+template <int N>
+struct AppendBatchT {
     int32_t count;
     int32_t max_n;
     int32_t layer0;       // first layer written
     int32_t total_rows;   // rows per layer in the packed input (A2T_ALL_LAYERS stride)
-    AppendDesc d[kMaxDesc];
+    AppendDesc d[N];
 };
+using AppendBatch = AppendBatchT<kMaxDesc>;
 
 // ---- attention (chunk and decode)
 struct AttnDesc {
@@ -78,15 +89,19 @@ struct AttnDesc {
     int32_t q_row0;    // first row of this stream in the packed q/o
     int32_t rope_row0; // row of the first query in the step's rotary table
     int32_t splits;    // key splits; 1 = write o directly
+    int32_t n_new;     // fused append: the last n_new keys come from the input k/v (else 0)
+    int32_t in_row0;   // fused append: first row of this stream in the input k/v
     int64_t ws_off;    // float offset of this stream's partials in the workspace
 };
-struct AttnBatch {
+template <int N>
+struct AttnBatchT {
     int32_t count;
     int32_t layer;
     int32_t max_splits;
     int32_t max_rows;  // max n_q over the batch
-    AttnDesc d[kMaxDesc];
+    AttnDesc d[N];
 };
+using AttnBatch = AttnBatchT<kMaxDesc>;
 
 // ---- eviction / compaction
 struct EvictDesc {
@@ -98,19 +113,32 @@ struct EvictDesc {
     int32_t u_last;    // newest evicted unit id
     int32_t n_keep;    // rows of the span that are retained (moved to the kept region)
 };
-struct EvictBatch {
+template <int N>
+struct EvictBatchT {
     int32_t count;
-    EvictDesc d[kMaxDesc];
+    EvictDesc d[N];
 };
+using EvictBatch = EvictBatchT<kMaxDesc>;
+
+// Kernel arguments are copied per launch: a launch carries a batch sized to
+// its stream count (1, 8 or kMaxDesc descriptors), not always the largest.
+template <template <int> class BT, int N>
+inline BT<N> shrink_batch(const BT<kMaxDesc>& b) {
+    BT<N> s;
+    static_assert(offsetof(BT<N>, d) == offsetof(BT<kMaxDesc>, d), "batch header layout");
+    std::memcpy(&s, &b, offsetof(BT<N>, d) + sizeof(b.d[0]) * (b.count < N ? b.count : N));
+    return s;
+}
 
 // Launchers (kernels.hip).  Each returns the hipError_t of the launch.
 hipError_t launch_step_meta(const DevState& st, const StepBatch& b, const uint8_t* seg,
                             const int32_t* pos, const int32_t* uid, hipStream_t stream);
 hipError_t launch_append(const DevState& st, const AppendBatch& b, int n_layers,
                          const void* k, const void* v, hipStream_t stream);
-// MFMA chunk attention (bf16 cache, D 64 or 128).
+// MFMA chunk attention (bf16 cache, D 64 or 128).  With k_in/v_in non-null it
+// also appends each stream's n_new newest rows (rotating K) from that input.
 hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* q, void* o,
-                            hipStream_t stream);
+                            const void* k_in, const void* v_in, hipStream_t stream);
 // VALU attention, one (row, kv head) per workgroup column (fp32 caches, decode).
 hipError_t launch_attn_valu(const DevState& st, const AttnBatch& b, const void* q, void* o,
                             hipStream_t stream);

@@ -21,6 +21,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace a2t {
 namespace {
 
@@ -67,64 +69,114 @@ __device__ __forceinline__ int64_t key_row(const DevState& st, int layer, int s,
     return pool_index(st, layer, s, g, st.unit_rows, slot);
 }
 
+// 8 consecutive elements <-> fp32, with one or two 16-byte accesses.
+__device__ __forceinline__ void load8(const float* p, float x[8]) {
+    const float4 a = reinterpret_cast<const float4*>(p)[0];
+    const float4 b = reinterpret_cast<const float4*>(p)[1];
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ __forceinline__ void load8(const bf16_t* p, float x[8]) {
+    const uint4 r = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        x[2 * e] = __uint_as_float(w[e] << 16);
+        x[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void store8(float* p, const float x[8]) {
+    reinterpret_cast<float4*>(p)[0] = make_float4(x[0], x[1], x[2], x[3]);
+    reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float x[8]) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)f32_to_bf16(x[2 * e]) | ((uint32_t)f32_to_bf16(x[2 * e + 1]) << 16);
+    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ void copy8(float* d, const float* s) {
+    reinterpret_cast<float4*>(d)[0] = reinterpret_cast<const float4*>(s)[0];
+    reinterpret_cast<float4*>(d)[1] = reinterpret_cast<const float4*>(s)[1];
+}
+__device__ __forceinline__ void copy8(bf16_t* d, const bf16_t* s) {
+    *reinterpret_cast<uint4*>(d) = *reinterpret_cast<const uint4*>(s);
+}
+
 // ------------------------------------------------------------------ step_meta
-__global__ __launch_bounds__(256) void step_meta_kernel(DevState st, StepBatch b,
-                                                        const uint8_t* seg, const int32_t* pos,
-                                                        const int32_t* uid) {
-    __shared__ int32_t s_pos[1024];
-    const StepDesc d = b.d[blockIdx.x];
-    const int64_t mb = (int64_t)d.s * st.unit_rows;
-    const int u = uid[blockIdx.x];
-    for (int r = threadIdx.x; r < d.n; r += blockDim.x) {
-        const int p = pos[d.row0 + r];
-        s_pos[r] = p;
+// grid (row, stream): one workgroup per new row, one thread per rotary pair.
+template <class BT>
+__global__ __launch_bounds__(64) void step_meta_kernel(DevState st, BT b,
+                                                       const uint8_t* seg, const int32_t* pos,
+                                                       const int32_t* uid) {
+    const StepDesc d = b.d[blockIdx.y];
+    const int r = blockIdx.x;
+    if (r >= d.n) return;
+    const int p = pos[d.row0 + r];
+    const int half = st.D / 2;
+    if (threadIdx.x == 0) {
         int slot = d.slot0 + r;
         if (slot >= st.unit_rows) slot -= st.unit_rows;
+        const int64_t mb = (int64_t)d.s * st.unit_rows;
         st.unit_pos[mb + slot] = p;
         st.unit_seg[mb + slot] = seg[d.row0 + r];
-        st.unit_uid[mb + slot] = u;
+        st.unit_uid[mb + slot] = uid[blockIdx.y];
     }
-    __syncthreads();
-    const int half = st.D / 2;
-    float2* tab = st.rope + (int64_t)d.s * st.max_step_rows * half;
-    for (int idx = threadIdx.x; idx < d.n * half; idx += blockDim.x) {
-        const int r = idx / half, i = idx - r * half;
+    const int i = threadIdx.x;
+    if (i < half) {
         const double inv = pow(st.theta, (-2.0 * i) / st.D);
-        const double a = (double)s_pos[r] * inv;
         double sn, cs;
-        sincos(a, &sn, &cs);
-        tab[idx] = make_float2((float)cs, (float)sn);
+        sincos((double)p * inv, &sn, &cs);
+        st.rope[((int64_t)d.s * st.max_step_rows + r) * half + i] = make_float2((float)cs, (float)sn);
     }
 }
 
 // --------------------------------------------------------------------- append
-template <typename T>
-__global__ __launch_bounds__(256) void append_kernel(DevState st, AppendBatch b, const T* k,
+// One thread per 8-element chunk of a new row (all heads, all rows of the
+// batch); every thread issues its loads at once, then writes its chunk.
+template <typename T, class BT>
+__global__ __launch_bounds__(256) void append_kernel(DevState st, BT b, const T* k,
                                                      const T* v) {
-    const int r = blockIdx.x;
     const AppendDesc d = b.d[blockIdx.y];
-    if (r >= d.n) return;
-    const int layer = b.layer0 + blockIdx.z;
     const int D = st.D, half = D / 2, Hkv = st.Hkv;
+    const int cph = D / 8;              // chunks per head row
+    const int cpr = Hkv * cph;          // chunks per row
+    const int q = blockIdx.x * blockDim.x + threadIdx.x;
+    const int r = q / cpr;
+    if (r >= d.n) return;
+    const int c = q - r * cpr;
+    const int g = c / cph, d0 = (c - g * cph) * 8;
+    const int layer = b.layer0 + blockIdx.z;
     int slot = d.slot0 + r;
     if (slot >= st.unit_rows) slot -= st.unit_rows;
-    const int64_t in = ((int64_t)blockIdx.z * b.total_rows + d.in_row0 + r) * Hkv * D;
-    const float2* cs = st.rope + ((int64_t)d.s * st.max_step_rows + r) * half;
-    T* kd = reinterpret_cast<T*>(st.k_unit);
-    T* vd = reinterpret_cast<T*>(st.v_unit);
-    for (int idx = threadIdx.x; idx < Hkv * half; idx += blockDim.x) {
-        const int g = idx / half, i = idx - g * half;
-        const float x1 = Elt<T>::load(k + in + g * D + i);
-        const float x2 = Elt<T>::load(k + in + g * D + i + half);
-        const float2 c = cs[i];
-        const int64_t o = pool_index(st, layer, d.s, g, st.unit_rows, slot);
-        Elt<T>::store(kd + o + i, x1 * c.x - x2 * c.y);
-        Elt<T>::store(kd + o + i + half, x2 * c.x + x1 * c.y);
+    const int64_t in = ((int64_t)blockIdx.z * b.total_rows + d.in_row0 + r) * Hkv * D + g * D;
+    const bool lower = d0 < half;
+    const int i0 = lower ? d0 : d0 - half;
+    const float4* cs4 = reinterpret_cast<const float4*>(
+        st.rope + ((int64_t)d.s * st.max_step_rows + r) * half + i0);
+    float x[8], y[8];
+    load8(k + in + d0, x);
+    load8(k + in + (lower ? d0 + half : d0 - half), y);
+    float4 cs[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) cs[e] = cs4[e];
+    const int64_t o = pool_index(st, layer, d.s, g, st.unit_rows, slot) + d0;
+    copy8(reinterpret_cast<T*>(st.v_unit) + o, v + in + d0);
+    float out[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        // cs[e] = (cos, sin) of pairs i0+2e and i0+2e+1
+        const float c0 = cs[e].x, s0 = cs[e].y, c1 = cs[e].z, s1 = cs[e].w;
+        if (lower) {
+            out[2 * e] = x[2 * e] * c0 - y[2 * e] * s0;
+            out[2 * e + 1] = x[2 * e + 1] * c1 - y[2 * e + 1] * s1;
+        } else {
+            out[2 * e] = x[2 * e] * c0 + y[2 * e] * s0;
+            out[2 * e + 1] = x[2 * e + 1] * c1 + y[2 * e + 1] * s1;
+        }
     }
-    for (int idx = threadIdx.x; idx < Hkv * D; idx += blockDim.x) {
-        const int g = idx / D, e = idx - g * D;
-        vd[pool_index(st, layer, d.s, g, st.unit_rows, slot) + e] = v[in + idx];
-    }
+    store8(reinterpret_cast<T*>(st.k_unit) + o, out);
 }
 
 // ----------------------------------------------------------------- attn_valu
@@ -132,8 +184,8 @@ __global__ __launch_bounds__(256) void append_kernel(DevState st, AppendBatch b,
 // form 16 key groups of 16 lanes; a lane holds D/16 consecutive elements of a
 // row.  Scores are reduced across the 16 lanes with xor shuffles; every key
 // group runs its own online softmax, and the 16 states are merged in LDS.
-template <typename T, int D, int G>
-__global__ __launch_bounds__(256) void attn_valu_kernel(DevState st, AttnBatch b, const T* q,
+template <typename T, int D, int G, class BT>
+__global__ __launch_bounds__(256) void attn_valu_kernel(DevState st, BT b, const T* q,
                                                         T* o) {
     constexpr int DPL = D / 16;
     __shared__ float s_m[16], s_l[16];
@@ -256,11 +308,11 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(DevState st, AttnBatch b
 }
 
 // ----------------------------------------------------------------- attn_mfma
-// One workgroup = (key split, kv head g, stream), 4 waves.  The M = G*n_q
-// query rows of the head group are processed 128 at a time; each wave owns 32
-// of them (two 16-column blocks).  Per 64-key tile, K (row-major) and V^T are
-// staged in LDS by all 256 threads, with the next tile's global loads issued
-// before the current tile's math.
+// One workgroup = (key split, kv head g, stream), 8 waves.  The M = G*n_q
+// query rows of the head group are processed 128 at a time; each wave owns 16
+// of them.  Per 64-key tile, K (row-major) and V^T are staged in LDS by all
+// 512 threads, with the next tile's global loads issued before the current
+// tile's math.
 //
 // S^T = K . Q^T with mfma_f32_16x16x32_bf16: A = K rows (16 keys x 32 dims),
 // B = Q^T (32 dims x 16 queries); the accumulator gives lane l the scores of
@@ -268,16 +320,44 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(DevState st, AttnBatch b
 // B operand of O^T = V^T . P^T: within a 32-key chunk, k-slot 8*(l/16)+j maps
 // to key 16*(j/4) + 4*(l/16) + j%4, which is exactly what lane l holds; the A
 // operand reads the same keys from V^T in LDS.  No cross-lane transposes.
-template <int D>
-__global__ __launch_bounds__(256) void attn_mfma_kernel(DevState st, AttnBatch b,
-                                                        const uint16_t* q, uint16_t* o) {
+constexpr int kMfmaThreads = 512;
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+    const bf16x2 v = {(__bf16)a, (__bf16)b};   // v_cvt_pk_bf16_f32, round to nearest even
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// max / sum over the four lanes l, l^16, l^32, l^48 (the lanes holding one
+// query column of a 16x16 accumulator), with the gfx950 row-swap permutes
+__device__ __forceinline__ float quad_max(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float quad_sum(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+template <int D, class BT>
+__global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT b,
+                                                                 const uint16_t* q, uint16_t* o,
+                                                                 const uint16_t* k_in,
+                                                                 const uint16_t* v_in) {
     constexpr int KS = D / 32;      // k-steps of Q.K^T
     constexpr int DB = D / 16;      // 16-row blocks of V^T
     constexpr int CPR = D / 8;      // 16-byte chunks per K/V row
     constexpr int KROW = D + 8;     // LDS row stride of K (bf16 elements)
-    constexpr int VROW = kTileKeys + 8;  // LDS row stride of V^T
-    constexpr int NK = kTileKeys * CPR / 256;         // K chunks per thread
-    constexpr int NVQ = (kTileKeys / 4) * CPR;        // V (4-key x 8-dim) blocks per tile
+    constexpr int VROW = kTileKeys + 8;              // LDS row stride of V^T
+    constexpr int NK = kTileKeys * CPR / kMfmaThreads;  // K chunks per thread
+    constexpr int NVP = (kTileKeys / 2) * CPR;          // V (2-key x 8-dim) blocks per tile
+    constexpr int QPW = 16;                             // queries per wave
+    constexpr int QPP = QPW * (kMfmaThreads / 64);      // queries per pass
+    static_assert(NK >= 1 && NVP <= kMfmaThreads, "tile shape");
     __shared__ __attribute__((aligned(16))) uint16_t Ks[kTileKeys * KROW];
     __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VROW];
 
@@ -289,106 +369,189 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(DevState st, AttnBatch b
     const int n_tiles = (R + kTileKeys - 1) / kTileKeys;
     const int t0 = sp * n_tiles / d.splits, t1 = (sp + 1) * n_tiles / d.splits;
     const int vis0 = R - nq;  // query row i sees keys 0 .. vis0 + i
+    const int kept = d.kept, head = d.head, ring_rows = st.unit_rows;
+    // fused append: keys newbase .. R-1 are this step's rows, read from the input
+    const int newbase = R - d.n_new;
 
-    const uint16_t* kk = reinterpret_cast<const uint16_t*>(st.k_kept);
-    const uint16_t* vk = reinterpret_cast<const uint16_t*>(st.v_kept);
-    const uint16_t* ku = reinterpret_cast<const uint16_t*>(st.k_unit);
-    const uint16_t* vu = reinterpret_cast<const uint16_t*>(st.v_unit);
+    const uint16_t* kk = reinterpret_cast<const uint16_t*>(st.k_kept) +
+                         pool_index(st, b.layer, d.s, g, st.kept_rows, 0);
+    const uint16_t* vk = reinterpret_cast<const uint16_t*>(st.v_kept) +
+                         pool_index(st, b.layer, d.s, g, st.kept_rows, 0);
+    const uint16_t* ku = reinterpret_cast<const uint16_t*>(st.k_unit) +
+                         pool_index(st, b.layer, d.s, g, st.unit_rows, 0);
+    const uint16_t* vu = reinterpret_cast<const uint16_t*>(st.v_unit) +
+                         pool_index(st, b.layer, d.s, g, st.unit_rows, 0);
+    // element offset of logical key j's row inside its region
+    auto row_off = [&](int j, bool* in_kept) -> int {
+        if (j < kept) {
+            *in_kept = true;
+            return j * D;
+        }
+        int slot = head + (j - kept);
+        if (slot >= ring_rows) slot -= ring_rows;
+        *in_kept = false;
+        return slot * D;
+    };
 
-    uint4 kreg[NK];
-    uint4 vreg[4];
+    // two register stages: the loads of the next two tiles are in flight while
+    // the current tile is computed
+    struct Stage {
+        uint4 k[NK];
+        uint4 kp[NK];  // rotate-half partner chunk of a new (not yet rotated) key row
+        uint4 v[2];
+    };
+    Stage sa, sb;
+    const int vkp = tid / CPR, vdc = tid - (tid / CPR) * CPR;  // V block: keys 2*vkp, 2*vkp+1
 
-    auto gload = [&](int t) {
+    auto gload = [&](int t, Stage& sg) {
+        uint4* kreg = sg.k;
+        uint4* vreg = sg.v;
+        uint4* kpart = sg.kp;
         const int kb = t * kTileKeys;
 #pragma unroll
         for (int it = 0; it < NK; ++it) {
-            const int c = tid + 256 * it;
+            const int c = tid + kMfmaThreads * it;
             const int row = c / CPR, col = c - row * CPR;
             const int j = kb + row;
-            if (j < R) {
-                bool in_kept;
-                const int64_t r = key_row(st, b.layer, d.s, g, d.kept, d.head, j, &in_kept);
-                kreg[it] = *reinterpret_cast<const uint4*>((in_kept ? kk : ku) + r + col * 8);
+            if (j >= newbase && j < R) {
+                const uint16_t* src = k_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D;
+                kreg[it] = *reinterpret_cast<const uint4*>(src + col * 8);
+                kpart[it] = *reinterpret_cast<const uint4*>(src + ((col * 8) ^ (D / 2)));
+            } else if (j < R) {
+                bool ik;
+                const int off = row_off(j, &ik);
+                kreg[it] = *reinterpret_cast<const uint4*>((ik ? kk : ku) + off + col * 8);
             } else {
                 kreg[it] = make_uint4(0, 0, 0, 0);
             }
         }
-        if (tid < NVQ) {
-            const int kq = tid / CPR, dc = tid - kq * CPR;
+        if (tid < NVP) {
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) {
-                const int j = kb + 4 * kq + r4;
-                if (j < R) {
-                    bool in_kept;
-                    const int64_t r = key_row(st, b.layer, d.s, g, d.kept, d.head, j, &in_kept);
-                    vreg[r4] = *reinterpret_cast<const uint4*>((in_kept ? vk : vu) + r + dc * 8);
+            for (int r2 = 0; r2 < 2; ++r2) {
+                const int j = kb + 2 * vkp + r2;
+                if (j >= newbase && j < R) {
+                    vreg[r2] = *reinterpret_cast<const uint4*>(
+                        v_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D + vdc * 8);
+                } else if (j < R) {
+                    bool ik;
+                    const int off = row_off(j, &ik);
+                    vreg[r2] = *reinterpret_cast<const uint4*>((ik ? vk : vu) + off + vdc * 8);
                 } else {
-                    vreg[r4] = make_uint4(0, 0, 0, 0);
+                    vreg[r2] = make_uint4(0, 0, 0, 0);
                 }
             }
         }
     };
-    auto lstore = [&]() {
+    auto lstore = [&](int t, const Stage& sg) {
+        const uint4* kreg = sg.k;
+        const uint4* vreg = sg.v;
+        const int kb = t * kTileKeys;
 #pragma unroll
         for (int it = 0; it < NK; ++it) {
-            const int c = tid + 256 * it;
+            const int c = tid + kMfmaThreads * it;
             const int row = c / CPR, col = c - row * CPR;
-            *reinterpret_cast<uint4*>(&Ks[row * KROW + col * 8]) = kreg[it];
+            const int j = kb + row;
+            uint4 kv = kreg[it];
+            if (j >= newbase && j < R) {
+                // fused append: rotate this new key chunk, then also store it to its ring slot
+                const int d0 = col * 8;
+                const bool lower = d0 < D / 2;
+                const int i0 = lower ? d0 : d0 - D / 2;
+                const float4* cs4 = reinterpret_cast<const float4*>(
+                    st.rope + ((int64_t)d.s * st.max_step_rows + (j - newbase)) * (D / 2) + i0);
+                const uint32_t xw[4] = {kv.x, kv.y, kv.z, kv.w};
+                const uint4 pv = sg.kp[it];
+                const uint32_t yw[4] = {pv.x, pv.y, pv.z, pv.w};
+                uint32_t ow[4];
+#pragma unroll
+                for (int e2 = 0; e2 < 4; ++e2) {
+                    const float4 c4 = cs4[e2];
+                    const float x0 = __uint_as_float(xw[e2] << 16), x1 = __uint_as_float(xw[e2] & 0xffff0000u);
+                    const float y0 = __uint_as_float(yw[e2] << 16), y1 = __uint_as_float(yw[e2] & 0xffff0000u);
+                    const float r0 = lower ? x0 * c4.x - y0 * c4.y : x0 * c4.x + y0 * c4.y;
+                    const float r1 = lower ? x1 * c4.z - y1 * c4.w : x1 * c4.z + y1 * c4.w;
+                    ow[e2] = pack_bf16x2(r0, r1);
+                }
+                kv = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+                bool ik;
+                const int off = row_off(j, &ik);
+                *reinterpret_cast<uint4*>(const_cast<uint16_t*>(ku) + off + d0) = kv;
+            }
+            *reinterpret_cast<uint4*>(&Ks[row * KROW + col * 8]) = kv;
         }
-        if (tid < NVQ) {
-            const int kq = tid / CPR, dc = tid - kq * CPR;
-            const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-            const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-            const uint32_t* v2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
-            const uint32_t* v3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
+        if (tid < NVP) {
+            // keys 2*vkp, 2*vkp+1 go to their k-slot positions: within a 32-key
+            // chunk, key 16h + 4q + e sits at 8q + 4h + e, so the 8 k-slots a
+            // lane feeds to one MFMA are contiguous in a V^T row
+            // The 16-byte chunks of a V^T row are XOR-swizzled by (row / 8) so that
+            // lanes writing different rows 8 apart land in different LDS banks.
+            const int kk = 2 * vkp, cch = kk >> 5, k = kk & 31;
+            const int vpos = 32 * cch + 8 * ((k & 15) >> 2) + 4 * (k >> 4) + (k & 3);
+            const uint32_t w0[4] = {vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w};
+            const uint32_t w1[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
+#pragma unroll
+            for (int r2 = 0; r2 < 2; ++r2) {
+                const int j = kb + kk + r2;
+                if (j >= newbase && j < R) {  // fused append: V row chunk to its ring slot
+                    bool ik;
+                    const int off = row_off(j, &ik);
+                    *reinterpret_cast<uint4*>(const_cast<uint16_t*>(vu) + off + vdc * 8) = vreg[r2];
+                }
+            }
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int wd = e >> 1;
-                uint32_t a, c2;
-                if ((e & 1) == 0) {
-                    a = (v0[wd] & 0xffffu) | (v1[wd] << 16);
-                    c2 = (v2[wd] & 0xffffu) | (v3[wd] << 16);
-                } else {
-                    a = (v0[wd] >> 16) | (v1[wd] & 0xffff0000u);
-                    c2 = (v2[wd] >> 16) | (v3[wd] & 0xffff0000u);
-                }
-                *reinterpret_cast<uint2*>(&Vt[(dc * 8 + e) * VROW + 4 * kq]) = make_uint2(a, c2);
+                const int row = vdc * 8 + e;
+                const int spos = ((((vpos >> 3) ^ (row >> 3)) & 7) << 3) | (vpos & 7);
+                const uint32_t pr = (e & 1) ? ((w0[wd] >> 16) | (w1[wd] & 0xffff0000u))
+                                            : ((w0[wd] & 0xffffu) | (w1[wd] << 16));
+                *reinterpret_cast<uint32_t*>(&Vt[row * VROW + spos]) = pr;
             }
         }
     };
 
     const float2* rope = st.rope + ((int64_t)d.s * st.max_step_rows + d.rope_row0) * (D / 2);
 
-    for (int qg0 = 0; qg0 < M; qg0 += 128) {
-        const int mw = qg0 + 32 * w;
+    for (int qg0 = 0; qg0 < M; qg0 += QPP) {
+        const int mw = qg0 + QPW * w;
         const bool active = mw < M;
+        // the first tile's loads go out before the Q prologue so both latencies overlap
+        if (t0 < t1) gload(t0, sa);
+        if (t0 + 1 < t1) gload(t0 + 1, sb);
 
         // Q^T operand: rotated, scaled by scale*log2(e), bf16.
-        bf16x8 qop[2][KS];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            const int mq = mw + 16 * qb + l16;
+        bf16x8 qop[KS];
+        {
+            const int mq = mw + l16;
             float x[KS][8];
             if (mq < M) {
                 const int i = mq / G, hh = mq - i * G;
                 const uint16_t* qp = q + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
+                const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)i * (D / 2));
+                float4 cs[KS / 2][4];
+#pragma unroll
+                for (int s = 0; s < KS / 2; ++s)
+#pragma unroll
+                    for (int e2 = 0; e2 < 4; ++e2) cs[s][e2] = cs4[(32 * s + 8 * lg) / 2 + e2];
 #pragma unroll
                 for (int s = 0; s < KS; ++s) {
                     const uint4 raw = *reinterpret_cast<const uint4*>(qp + 32 * s + 8 * lg);
-                    const uint32_t* rw = reinterpret_cast<const uint32_t*>(&raw);
+                    const uint32_t rw[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        x[s][e] = bf16_to_f32((uint16_t)(rw[e >> 1] >> (16 * (e & 1))));
+                    for (int e = 0; e < 4; ++e) {
+                        x[s][2 * e] = __uint_as_float(rw[e] << 16);
+                        x[s][2 * e + 1] = __uint_as_float(rw[e] & 0xffff0000u);
+                    }
                 }
-                const float2* cs = rope + (int64_t)i * (D / 2);
 #pragma unroll
                 for (int s = 0; s < KS / 2; ++s) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        const float2 c = cs[32 * s + 8 * lg + e];
+                        const float4 c4 = cs[s][e >> 1];
+                        const float cc = (e & 1) ? c4.z : c4.x, sn = (e & 1) ? c4.w : c4.y;
                         const float a = x[s][e], bb = x[s + KS / 2][e];
-                        x[s][e] = (a * c.x - bb * c.y) * st.scale_log2e;
-                        x[s + KS / 2][e] = (bb * c.x + a * c.y) * st.scale_log2e;
+                        x[s][e] = (a * cc - bb * sn) * st.scale_log2e;
+                        x[s + KS / 2][e] = (bb * cc + a * sn) * st.scale_log2e;
                     }
                 }
             } else {
@@ -398,148 +561,123 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(DevState st, AttnBatch b
                     for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
             }
 #pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                uint32_t pk[4];
-#pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2)
-                    pk[e2] = (uint32_t)f32_to_bf16(x[s][2 * e2]) |
-                             ((uint32_t)f32_to_bf16(x[s][2 * e2 + 1]) << 16);
-                qop[qb][s] = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
-            }
+            for (int s = 0; s < KS; ++s)
+                qop[s] = __builtin_bit_cast(
+                    bf16x8, make_uint4(pack_bf16x2(x[s][0], x[s][1]), pack_bf16x2(x[s][2], x[s][3]),
+                                       pack_bf16x2(x[s][4], x[s][5]), pack_bf16x2(x[s][6], x[s][7])));
         }
 
-        float mrun[2] = {-INFINITY, -INFINITY}, lrun[2] = {0.f, 0.f};
-        f32x4 acc[DB][2];
+        float mrun = -INFINITY, lrun = 0.f;
+        f32x4 acc[DB];
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) acc[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int mq = mw + l16;
+        const int lim = (mq < M) ? vis0 + mq / G : -1;
 
-        if (t0 < t1) gload(t0);
-        for (int t = t0; t < t1; ++t) {
-            __syncthreads();  // every wave is done reading the previous tile
-            lstore();
-            __syncthreads();
-            if (t + 1 < t1) gload(t + 1);
-            if (!active) continue;
+        auto compute = [&](int t) {
             const int kbase = t * kTileKeys;
 
-            f32x4 sacc[4][2];
+            f32x4 sacc[4];
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int qb = 0; qb < 2; ++qb) sacc[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int kb = 0; kb < 4; ++kb) sacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
 #pragma unroll
                 for (int kb = 0; kb < 4; ++kb) {
                     const bf16x8 a = *reinterpret_cast<const bf16x8*>(
                         &Ks[(kb * 16 + l16) * KROW + 32 * s + 8 * lg]);
-#pragma unroll
-                    for (int qb = 0; qb < 2; ++qb)
-                        sacc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            a, qop[qb][s], sacc[kb][qb], 0, 0, 0);
+                    sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[s], sacc[kb], 0, 0, 0);
                 }
             }
             if (kbase + kTileKeys - 1 > vis0) {
 #pragma unroll
-                for (int qb = 0; qb < 2; ++qb) {
-                    const int mq = mw + 16 * qb + l16;
-                    const int lim = (mq < M) ? vis0 + mq / G : -1;
-#pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const int j = kbase + kb * 16 + 4 * lg + e;
-                            if (j > lim) sacc[kb][qb][e] = -INFINITY;
-                        }
-                }
-            }
-
-            bf16x8 pop[2][2];
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) {
-                float tmax = -INFINITY;
-#pragma unroll
                 for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, sacc[kb][qb][e]);
-                tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-                tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-                const float mn = fmaxf(mrun[qb], tmax);
-                const float mu = (mn == -INFINITY) ? 0.f : mn;
-                const float corr = exp2f(mrun[qb] - mu);
-                float rs = 0.f;
-                uint32_t pk[4][2];
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    uint16_t h[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        h[e] = f32_to_bf16(exp2f(sacc[kb][qb][e] - mu));
-                        rs += bf16_to_f32(h[e]);
-                    }
-                    pk[kb][0] = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-                    pk[kb][1] = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-                }
-                rs += __shfl_xor(rs, 16);
-                rs += __shfl_xor(rs, 32);
-                lrun[qb] = lrun[qb] * corr + rs;
-                mrun[qb] = mn;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) acc[db][qb] *= corr;
-#pragma unroll
-                for (int c = 0; c < 2; ++c)
-                    pop[c][qb] = __builtin_bit_cast(
-                        bf16x8, make_uint4(pk[2 * c][0], pk[2 * c][1], pk[2 * c + 1][0],
-                                           pk[2 * c + 1][1]));
+                    for (int e = 0; e < 4; ++e)
+                        if (kbase + kb * 16 + 4 * lg + e > lim) sacc[kb][e] = -INFINITY;
             }
+
+            float tmax = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, sacc[kb][e]);
+            tmax = quad_max(tmax);
+            const float mn = fmaxf(mrun, tmax);
+            const float mu = (mn == -INFINITY) ? 0.f : mn;
+            if (__any(mn != mrun)) {
+                const float corr = __builtin_amdgcn_exp2f(mrun - mu);
+                lrun *= corr;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) acc[db] *= corr;
+            }
+            mrun = mn;
+            uint32_t pk[4][2];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                float p[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    p[e] = __builtin_amdgcn_exp2f(sacc[kb][e] - mu);
+                    lrun += p[e];  // this lane's share of the row sum
+                }
+                pk[kb][0] = pack_bf16x2(p[0], p[1]);
+                pk[kb][1] = pack_bf16x2(p[2], p[3]);
+            }
+            bf16x8 pop[2];
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+                pop[c] = __builtin_bit_cast(
+                    bf16x8, make_uint4(pk[2 * c][0], pk[2 * c][1], pk[2 * c + 1][0], pk[2 * c + 1][1]));
 
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
-                    const uint16_t* vr = &Vt[(db * 16 + l16) * VROW + 32 * c + 4 * lg];
-                    const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-                    const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-                    const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-#pragma unroll
-                    for (int qb = 0; qb < 2; ++qb)
-                        acc[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pop[c][qb],
-                                                                             acc[db][qb], 0, 0, 0);
+                    const int row = db * 16 + l16;
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                        &Vt[row * VROW + ((((4 * c + lg) ^ (row >> 3)) & 7) << 3)]);
+                    acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pop[c], acc[db], 0, 0, 0);
                 }
+            }
+        };
+        for (int t = t0; t < t1; t += 2) {
+            __syncthreads();  // every wave is done reading the previous tile
+            lstore(t, sa);
+            __syncthreads();
+            if (t + 2 < t1) gload(t + 2, sa);
+            if (active) compute(t);
+            if (t + 1 < t1) {
+                __syncthreads();
+                lstore(t + 1, sb);
+                __syncthreads();
+                if (t + 3 < t1) gload(t + 3, sb);
+                if (active) compute(t + 1);
             }
         }
 
-        if (active) {
+        if (active) lrun = quad_sum(lrun);
+        if (active && mq < M) {
+            const int i = mq / G, hh = mq - i * G;
+            if (d.splits == 1) {
+                const float inv = 1.f / lrun;
+                uint16_t* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb) {
-                const int mq = mw + 16 * qb + l16;
-                if (mq >= M) continue;
-                const int i = mq / G, hh = mq - i * G;
-                if (d.splits == 1) {
-                    const float inv = 1.f / lrun[qb];
-                    uint16_t* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
+                for (int db = 0; db < DB; ++db) {
+                    const f32x4 a = acc[db];
+                    *reinterpret_cast<uint2*>(op + db * 16 + 4 * lg) =
+                        make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
+                }
+            } else {
+                float* po = st.ws + d.ws_off;
+                float* prow = po + (((int64_t)sp * st.Hkv + g) * M + mq) * D;
 #pragma unroll
-                    for (int db = 0; db < DB; ++db) {
-                        const f32x4 a = acc[db][qb];
-                        const uint32_t lo = (uint32_t)f32_to_bf16(a[0] * inv) |
-                                            ((uint32_t)f32_to_bf16(a[1] * inv) << 16);
-                        const uint32_t hi = (uint32_t)f32_to_bf16(a[2] * inv) |
-                                            ((uint32_t)f32_to_bf16(a[3] * inv) << 16);
-                        *reinterpret_cast<uint2*>(op + db * 16 + 4 * lg) = make_uint2(lo, hi);
-                    }
-                } else {
-                    float* po = st.ws + d.ws_off;
-                    float* prow = po + (((int64_t)sp * st.Hkv + g) * M + mq) * D;
-#pragma unroll
-                    for (int db = 0; db < DB; ++db)
-                        *reinterpret_cast<f32x4*>(prow + db * 16 + 4 * lg) = acc[db][qb];
-                    if (lg == 0) {
-                        float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
-                        pml[(((int64_t)sp * st.Hkv + g) * M + mq) * 2 + 0] = mrun[qb];
-                        pml[(((int64_t)sp * st.Hkv + g) * M + mq) * 2 + 1] = lrun[qb];
-                    }
+                for (int db = 0; db < DB; ++db)
+                    *reinterpret_cast<f32x4*>(prow + db * 16 + 4 * lg) = acc[db];
+                if (lg == 0) {
+                    float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
+                    *reinterpret_cast<float2*>(pml + (((int64_t)sp * st.Hkv + g) * M + mq) * 2) =
+                        make_float2(mrun, lrun);
                 }
             }
         }
@@ -548,29 +686,64 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(DevState st, AttnBatch b
 }
 
 // ----------------------------------------------------------------- attn_merge
-template <typename T>
-__global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, AttnBatch b, T* o) {
+// grid (row blocks, kv head, stream); each thread owns 4 output elements of
+// one query row.  The splits are read 16 at a time (all loads of a batch in
+// flight together) and combined in fixed split order, so the result is
+// deterministic.
+template <typename T, class BT>
+__global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
+    constexpr int B = 16;
     const AttnDesc d = b.d[blockIdx.z];
     if (d.splits <= 1) return;
     const int G = st.Hq / st.Hkv, M = G * d.n_q, D = st.D, g = blockIdx.y;
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= M * D) return;
-    const int mq = idx / D, dd = idx - mq * D;
+    const int tpr = D / 4;           // threads per query row
+    const int rpb = 256 / tpr;       // query rows per block
+    const int rr = threadIdx.x / tpr, d4 = (threadIdx.x - rr * tpr) * 4;
+    const int mq = blockIdx.x * rpb + rr;
+    if (mq >= M) return;
     const float* po = st.ws + d.ws_off;
     const float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
-    float mx = -INFINITY;
-    for (int sp = 0; sp < d.splits; ++sp)
-        mx = fmaxf(mx, pml[(((int64_t)sp * st.Hkv + g) * M + mq) * 2]);
-    float L = 0.f, O = 0.f;
-    for (int sp = 0; sp < d.splits; ++sp) {
-        const int64_t r = ((int64_t)sp * st.Hkv + g) * M + mq;
-        const float ms = pml[r * 2];
-        const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - mx);
-        L += wgt * pml[r * 2 + 1];
-        O += wgt * po[r * D + dd];
+    const int64_t ostride = (int64_t)st.Hkv * M * D, mstride = (int64_t)st.Hkv * M * 2;
+    const float* orow = po + ((int64_t)g * M + mq) * D + d4;
+    const float* mrow = pml + ((int64_t)g * M + mq) * 2;
+    float mx = -INFINITY, L = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < d.splits; s0 += B) {
+        float2 ml[B];
+        float4 ov[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            if (s0 + j < d.splits) {
+                ml[j] = *reinterpret_cast<const float2*>(mrow + (s0 + j) * mstride);
+                ov[j] = *reinterpret_cast<const float4*>(orow + (s0 + j) * ostride);
+            } else {
+                ml[j] = make_float2(-INFINITY, 0.f);
+                ov[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+        float bm = mx;
+#pragma unroll
+        for (int j = 0; j < B; ++j) bm = fmaxf(bm, ml[j].x);
+        if (bm == -INFINITY) continue;
+        const float c = (mx == -INFINITY) ? 0.f : exp2f(mx - bm);
+        L *= c;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) O[e] *= c;
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            const float w = (ml[j].x == -INFINITY) ? 0.f : exp2f(ml[j].x - bm);
+            L += w * ml[j].y;
+            O[0] += w * ov[j].x;
+            O[1] += w * ov[j].y;
+            O[2] += w * ov[j].z;
+            O[3] += w * ov[j].w;
+        }
+        mx = bm;
     }
+    const float inv = 1.f / L;
     const int i = mq / G, hh = mq - i * G;
-    Elt<T>::store(o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D + dd, O / L);
+    T* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D + d4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) Elt<T>::store(op + e, O[e] * inv);
 }
 
 // ---------------------------------------------------------------------- evict
@@ -579,8 +752,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, AttnBatch 
 // writes the kept-region metadata and the mask / compaction indices over the
 // whole pre-eviction cache.  Each workgroup ranks the span's rows itself
 // (wave ballot + popcount, then a cross-wave prefix in LDS).
-template <int ELT>
-__global__ __launch_bounds__(256) void evict_kernel(DevState st, EvictBatch b) {
+template <int ELT, class BT>
+__global__ __launch_bounds__(256) void evict_kernel(DevState st, BT b) {
     __shared__ int s_wave[4];
     __shared__ int s_src[256];
     __shared__ int s_dst[256];
@@ -673,49 +846,72 @@ __global__ __launch_bounds__(256) void evict_kernel(DevState st, EvictBatch b) {
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
+// Calls f with the batch shrunk to the smallest of 1, 8 or kMaxDesc descriptors.
+template <template <int> class BT, class F>
+static hipError_t by_size(const BT<kMaxDesc>& b, F&& f) {
+    if (b.count <= 1) return f(shrink_batch<BT, 1>(b));
+    if (b.count <= 8) return f(shrink_batch<BT, 8>(b));
+    return f(b);
+}
+
 hipError_t launch_step_meta(const DevState& st, const StepBatch& b, const uint8_t* seg,
                             const int32_t* pos, const int32_t* uid, hipStream_t stream) {
-    hipLaunchKernelGGL(step_meta_kernel, dim3(b.count), dim3(256), 0, stream, st, b, seg, pos, uid);
-    return hipGetLastError();
+    return by_size<StepBatchT>(b, [&](const auto& bb) {
+        using B = std::decay_t<decltype(bb)>;
+        hipLaunchKernelGGL((step_meta_kernel<B>), dim3(b.max_n, b.count), dim3(64), 0, stream, st, bb,
+                           seg, pos, uid);
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_append(const DevState& st, const AppendBatch& b, int n_layers, const void* k,
                          const void* v, hipStream_t stream) {
-    const dim3 grid(b.max_n, b.count, n_layers);
-    if (st.dtype == 0)
-        hipLaunchKernelGGL(append_kernel<float>, grid, dim3(128), 0, stream, st, b,
-                           static_cast<const float*>(k), static_cast<const float*>(v));
-    else
-        hipLaunchKernelGGL(append_kernel<bf16_t>, grid, dim3(128), 0, stream, st, b,
-                           static_cast<const bf16_t*>(k), static_cast<const bf16_t*>(v));
-    return hipGetLastError();
+    const int cpr = st.Hkv * st.D / 8;
+    const dim3 grid((b.max_n * cpr + 255) / 256, b.count, n_layers);
+    return by_size<AppendBatchT>(b, [&](const auto& bb) {
+        using B = std::decay_t<decltype(bb)>;
+        if (st.dtype == 0)
+            hipLaunchKernelGGL((append_kernel<float, B>), grid, dim3(256), 0, stream, st, bb,
+                               static_cast<const float*>(k), static_cast<const float*>(v));
+        else
+            hipLaunchKernelGGL((append_kernel<bf16_t, B>), grid, dim3(256), 0, stream, st, bb,
+                               static_cast<const bf16_t*>(k), static_cast<const bf16_t*>(v));
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* q, void* o,
-                            hipStream_t stream) {
+                            const void* k_in, const void* v_in, hipStream_t stream) {
+    const uint16_t* ki = static_cast<const uint16_t*>(k_in);
+    const uint16_t* vi = static_cast<const uint16_t*>(v_in);
     const dim3 grid(b.max_splits, st.Hkv, b.count);
     const uint16_t* qq = static_cast<const uint16_t*>(q);
     uint16_t* oo = static_cast<uint16_t*>(o);
-    if (st.D == 128)
-        hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(256), 0, stream, st, b, qq, oo);
-    else if (st.D == 64)
-        hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, stream, st, b, qq, oo);
-    else
-        return hipErrorInvalidValue;
-    return hipGetLastError();
+    return by_size<AttnBatchT>(b, [&](const auto& bb) {
+        using B = std::decay_t<decltype(bb)>;
+        if (st.D == 128)
+            hipLaunchKernelGGL((attn_mfma_kernel<128, B>), grid, dim3(kMfmaThreads), 0, stream, st, bb,
+                               qq, oo, ki, vi);
+        else if (st.D == 64)
+            hipLaunchKernelGGL((attn_mfma_kernel<64, B>), grid, dim3(kMfmaThreads), 0, stream, st, bb,
+                               qq, oo, ki, vi);
+        else
+            return hipErrorInvalidValue;
+        return hipGetLastError();
+    });
 }
 
-template <typename T, int D>
-static hipError_t valu_dispatch_g(const DevState& st, const AttnBatch& b, const void* q, void* o,
+template <typename T, int D, class B>
+static hipError_t valu_dispatch_g(const DevState& st, const B& b, const void* q, void* o,
                                   hipStream_t stream) {
     const dim3 grid(b.max_splits, st.Hkv * b.max_rows, b.count);
     const T* qq = static_cast<const T*>(q);
     T* oo = static_cast<T*>(o);
     switch (st.Hq / st.Hkv) {
-        case 1: hipLaunchKernelGGL((attn_valu_kernel<T, D, 1>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
-        case 2: hipLaunchKernelGGL((attn_valu_kernel<T, D, 2>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
-        case 4: hipLaunchKernelGGL((attn_valu_kernel<T, D, 4>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
-        case 8: hipLaunchKernelGGL((attn_valu_kernel<T, D, 8>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
+        case 1: hipLaunchKernelGGL((attn_valu_kernel<T, D, 1, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
+        case 2: hipLaunchKernelGGL((attn_valu_kernel<T, D, 2, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
+        case 4: hipLaunchKernelGGL((attn_valu_kernel<T, D, 4, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
+        case 8: hipLaunchKernelGGL((attn_valu_kernel<T, D, 8, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -723,36 +919,46 @@ static hipError_t valu_dispatch_g(const DevState& st, const AttnBatch& b, const 
 
 hipError_t launch_attn_valu(const DevState& st, const AttnBatch& b, const void* q, void* o,
                             hipStream_t stream) {
-    if (st.dtype == 0) {
-        if (st.D == 128) return valu_dispatch_g<float, 128>(st, b, q, o, stream);
-        if (st.D == 64) return valu_dispatch_g<float, 64>(st, b, q, o, stream);
-    } else {
-        if (st.D == 128) return valu_dispatch_g<bf16_t, 128>(st, b, q, o, stream);
-        if (st.D == 64) return valu_dispatch_g<bf16_t, 64>(st, b, q, o, stream);
-    }
-    return hipErrorInvalidValue;
+    return by_size<AttnBatchT>(b, [&](const auto& bb) {
+        using B = std::decay_t<decltype(bb)>;
+        if (st.dtype == 0) {
+            if (st.D == 128) return valu_dispatch_g<float, 128>(st, bb, q, o, stream);
+            if (st.D == 64) return valu_dispatch_g<float, 64>(st, bb, q, o, stream);
+        } else {
+            if (st.D == 128) return valu_dispatch_g<bf16_t, 128>(st, bb, q, o, stream);
+            if (st.D == 64) return valu_dispatch_g<bf16_t, 64>(st, bb, q, o, stream);
+        }
+        (void)sizeof(B);
+        return hipErrorInvalidValue;
+    });
 }
 
 hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hipStream_t stream) {
     const int G = st.Hq / st.Hkv;
-    const int max_elems = G * b.max_rows * st.D;
-    const dim3 grid((max_elems + 255) / 256, st.Hkv, b.count);
-    if (st.dtype == 0)
-        hipLaunchKernelGGL(attn_merge_kernel<float>, grid, dim3(256), 0, stream, st, b,
-                           static_cast<float*>(o));
-    else
-        hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, grid, dim3(256), 0, stream, st, b,
-                           static_cast<bf16_t*>(o));
-    return hipGetLastError();
+    const int rpb = 256 / (st.D / 4);
+    const dim3 grid((G * b.max_rows + rpb - 1) / rpb, st.Hkv, b.count);
+    return by_size<AttnBatchT>(b, [&](const auto& bb) {
+        using B = std::decay_t<decltype(bb)>;
+        if (st.dtype == 0)
+            hipLaunchKernelGGL((attn_merge_kernel<float, B>), grid, dim3(256), 0, stream, st, bb,
+                               static_cast<float*>(o));
+        else
+            hipLaunchKernelGGL((attn_merge_kernel<bf16_t, B>), grid, dim3(256), 0, stream, st, bb,
+                               static_cast<bf16_t*>(o));
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream) {
     const dim3 grid(st.L + 1, b.count);
-    if (st.dtype == 0)
-        hipLaunchKernelGGL(evict_kernel<4>, grid, dim3(256), 0, stream, st, b);
-    else
-        hipLaunchKernelGGL(evict_kernel<2>, grid, dim3(256), 0, stream, st, b);
-    return hipGetLastError();
+    return by_size<EvictBatchT>(b, [&](const auto& bb) {
+        using B = std::decay_t<decltype(bb)>;
+        if (st.dtype == 0)
+            hipLaunchKernelGGL((evict_kernel<4, B>), grid, dim3(256), 0, stream, st, bb);
+        else
+            hipLaunchKernelGGL((evict_kernel<2, B>), grid, dim3(256), 0, stream, st, bb);
+        return hipGetLastError();
+    });
 }
 
 }  // namespace a2t

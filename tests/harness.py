@@ -73,7 +73,7 @@ class Lockstep:
 
     def __init__(self, cfg, seed, specs, *, layers_checked, n_layers, budgets, window,
                  unit_rows, kept_rows, max_step, tol, dtype=None, check_kv_every=1,
-                 all_layers_append=False, query_rows=None):
+                 all_layers_append=False, query_rows=None, fused=False):
         from oracle.cache import OracleCache
         import paper_2609_31224_amd as a2t
         self.a2t = a2t
@@ -87,6 +87,7 @@ class Lockstep:
         self.check_kv_every = check_kv_every
         self.all_layers_append = all_layers_append
         self.query_rows = query_rows
+        self.fused = fused   # a2t_append_attn instead of a2t_append + a2t_chunk_attn
         self.cache = make_cache(cfg, len(specs), unit_rows, kept_rows, max_step, n_layers=n_layers,
                                 dtype=self.dtype)
         self.oracles = [OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, self.layers_checked,
@@ -146,10 +147,12 @@ class Lockstep:
             vv_ = self._upload(np.stack([packed("v", l) for l in range(self.n_layers)]))
             a2t.a2t_append(self.cache, a2t.A2T_ALL_LAYERS, ids, n, kk, vv_, seg, pos, unit)
         for layer in range(self.n_layers):
+            fuse = self.fused and not decode and not self.all_layers_append
             if not self.all_layers_append:
                 kk, vv_ = self._upload(packed("k", layer)), self._upload(packed("v", layer))
                 meta = (seg, pos, unit) if layer == 0 else (None, None, None)
-                a2t.a2t_append(self.cache, layer, ids, n, kk, vv_, *meta)
+                if not fuse:
+                    a2t.a2t_append(self.cache, layer, ids, n, kk, vv_, *meta)
             qfull = packed("q", layer)
             # queries: the last nq rows of every stream's step
             rows, off = [], 0
@@ -160,6 +163,8 @@ class Lockstep:
             o = torch.empty_like(q)
             if decode:
                 a2t.a2t_decode_attn(self.cache, layer, ids, q, o)
+            elif fuse:
+                a2t.a2t_append_attn(self.cache, layer, ids, n, kk, vv_, *meta, nq, q, o)
             else:
                 a2t.a2t_chunk_attn(self.cache, layer, ids, nq, q, o)
             if layer in self.layers_checked:

@@ -210,6 +210,65 @@ def test_runs_are_bit_identical(gpu):
     assert np.array_equal(outs[0], outs[1])
 
 
+@pytest.mark.parametrize("dtype,tol", [("f32", F32_TOL), ("bf16", BF16_TOL)])
+def test_fused_append_attention_config0(gpu, dtype, tol):
+    cfg = CONFIGS[0]
+    spec = make_workload(cfg, seed=2).streams[0]
+    ls = Lockstep(cfg, 2, [spec], layers_checked=[0, 1], n_layers=2, budgets=[cfg.budget],
+                  window=cfg.window, tol=tol, dtype=dtype, fused=True, query_rows=7,
+                  **_bounds([spec], cfg.budget))
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    _report(ls, f"fused cfg0 {dtype}")
+    assert ls.evictions > 40
+
+
+@pytest.mark.parametrize("splits", ["1", "5", "32"])
+def test_fused_append_attention_config1_shape(gpu, splits):
+    cfg = CONFIGS[1]
+    spec = make_workload(cfg, units=200).streams[0]
+    old = os.environ.get("A2T_SPLITS")
+    os.environ["A2T_SPLITS"] = splits
+    try:
+        ls = Lockstep(cfg, cfg.index, [spec], layers_checked=[0, 35], n_layers=36,
+                      budgets=[cfg.budget], window=cfg.window, tol=BF16_TOL, check_kv_every=10,
+                      fused=True, **_bounds([spec], cfg.budget))
+        try:
+            ls.run()
+        finally:
+            ls.close()
+    finally:
+        if old is None:
+            os.environ.pop("A2T_SPLITS", None)
+        else:
+            os.environ["A2T_SPLITS"] = old
+    _report(ls, f"fused cfg1 splits{splits}")
+    assert ls.evictions >= 10
+
+
+def test_fused_edges_and_varlen(gpu):
+    cfg = CONFIGS[0]
+    spec = tiny_stream(EDGE_UNITS, prefix=5, pos_gap=3)
+    ls = Lockstep(cfg, 11, [spec], layers_checked=[0, 1], n_layers=2, budgets=[40], window=1,
+                  tol=BF16_TOL, dtype="bf16", unit_rows=240, kept_rows=400, max_step=84, fused=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    cfg2 = CONFIGS[2]
+    w = make_workload(cfg2, n_streams=5, units=110)
+    ls = Lockstep(cfg2, cfg2.index, w.streams, layers_checked=[0, 35], n_layers=36,
+                  budgets=[s.budget // 4 for s in w.streams], window=cfg2.window, tol=BF16_TOL,
+                  check_kv_every=20, fused=True, **_bounds(w.streams, 1024))
+    try:
+        ls.run(offsets=[s.offset % 23 for s in w.streams])
+    finally:
+        ls.close()
+    _report(ls, "fused varlen")
+
+
 def test_errors_on_gpu_leave_cache_usable(gpu):
     import torch
     import paper_2609_31224_amd as a2t
