@@ -149,10 +149,12 @@ void prof_harvest(a2t_cache* c, bool wait) {
     }
 }
 
+// Times the one kernel that a launcher issues inside the scope: the launcher
+// takes kt() and records the events at the dispatch's own begin and end.
 struct ProfScope {
     a2t_cache* c;
     ProfEvent ev;
-    bool on = false;
+    KTimer t;
     ProfScope(a2t_cache* cc, const char* name) : c(cc) {
         if (!c->prof_on) return;
         if (!c->prof_filter.empty() && std::strstr(name, c->prof_filter.c_str()) == nullptr) return;
@@ -168,11 +170,12 @@ struct ProfScope {
         c->prof_free.pop_back();
         ev.start = c->prof_free.back();
         c->prof_free.pop_back();
-        on = hipEventRecord(ev.start, c->stream) == hipSuccess;
+        t.start = ev.start;
+        t.stop = ev.stop;
     }
+    const KTimer& kt() const { return t; }
     ~ProfScope() {
-        if (!on) return;
-        if (hipEventRecord(ev.stop, c->stream) == hipSuccess) c->prof_pending.push_back(ev);
+        if (t.start) c->prof_pending.push_back(ev);
     }
 };
 
@@ -273,13 +276,13 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     hipError_t e;
     {
         ProfScope ps(c, valu ? "attn_valu" : "attn_mfma");
-        e = valu ? launch_attn_valu(c->dev, b, q, o, c->stream)
-                 : launch_attn_mfma(c->dev, b, q, o, k_in, v_in, c->stream);
+        e = valu ? launch_attn_valu(c->dev, b, q, o, c->stream, ps.kt())
+                 : launch_attn_mfma(c->dev, b, q, o, k_in, v_in, c->stream, ps.kt());
     }
     if (e != hipSuccess) return hip_fail(c);
     if (splits > 1) {
         ProfScope ps(c, "attn_merge");
-        if (launch_attn_merge(c->dev, b, o, c->stream) != hipSuccess) return hip_fail(c);
+        if (launch_attn_merge(c->dev, b, o, c->stream, ps.kt()) != hipSuccess) return hip_fail(c);
     }
     return A2T_OK;
 }
@@ -603,7 +606,7 @@ static int append_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int
                 e = launch_step_meta(c->dev, sb, reinterpret_cast<const uint8_t*>(sseg) + shift,
                                      reinterpret_cast<const int32_t*>(reinterpret_cast<uint8_t*>(spos) + shift),
                                      reinterpret_cast<const int32_t*>(reinterpret_cast<uint8_t*>(suid) + shift),
-                                     c->stream);
+                                     c->stream, ps.kt());
             }
             if (e != hipSuccess || !stage_release(c, slot)) return hip_fail(c);
             row += rows_here;
@@ -630,7 +633,7 @@ static int append_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int
             {
                 ProfScope ps(c, "append");
                 e = launch_append(c->dev, ab, layer == A2T_ALL_LAYERS ? k.n_layers : 1, kin, vin,
-                                  c->stream);
+                                  c->stream, ps.kt());
             }
             if (e != hipSuccess) return hip_fail(c);
         }
@@ -739,7 +742,7 @@ int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t
             hipError_t e;
             {
                 ProfScope ps(c, "evict");
-                e = launch_evict(c->dev, eb, c->stream);
+                e = launch_evict(c->dev, eb, c->stream, ps.kt());
             }
             eb.count = 0;
             return e == hipSuccess ? A2T_OK : hip_fail(c);

@@ -130,20 +130,32 @@ inline BT<N> shrink_batch(const BT<kMaxDesc>& b) {
     return s;
 }
 
-// Launchers (kernels.hip).  Each returns the hipError_t of the launch.
+// Optional dispatch timestamps: with start non-null the launcher issues its one
+// kernel through hipExtLaunchKernel, which records start/stop at the kernel's
+// own begin and end (no extra packets on the stream between them).
+struct KTimer {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+
+// Launchers (kernels.hip).  Each issues one kernel and returns the hipError_t
+// of the launch.
 hipError_t launch_step_meta(const DevState& st, const StepBatch& b, const uint8_t* seg,
-                            const int32_t* pos, const int32_t* uid, hipStream_t stream);
+                            const int32_t* pos, const int32_t* uid, hipStream_t stream,
+                            const KTimer& kt);
 hipError_t launch_append(const DevState& st, const AppendBatch& b, int n_layers,
-                         const void* k, const void* v, hipStream_t stream);
+                         const void* k, const void* v, hipStream_t stream, const KTimer& kt);
 // MFMA chunk attention (bf16 cache, D 64 or 128).  With k_in/v_in non-null it
 // also appends each stream's n_new newest rows (rotating K) from that input.
 hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* q, void* o,
-                            const void* k_in, const void* v_in, hipStream_t stream);
+                            const void* k_in, const void* v_in, hipStream_t stream,
+                            const KTimer& kt);
 // VALU attention, one (row, kv head) per workgroup column (fp32 caches, decode).
 hipError_t launch_attn_valu(const DevState& st, const AttnBatch& b, const void* q, void* o,
-                            hipStream_t stream);
+                            hipStream_t stream, const KTimer& kt);
 hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o,
-                             hipStream_t stream);
-hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream);
+                             hipStream_t stream, const KTimer& kt);
+hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream,
+                        const KTimer& kt);
 
 }  // namespace a2t

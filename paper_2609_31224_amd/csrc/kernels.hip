@@ -19,6 +19,7 @@
 //               eviction mask and compaction indices over the whole cache.
 #include "a2t_internal.h"
 
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include <type_traits>
@@ -343,6 +344,25 @@ __device__ __forceinline__ float quad_sum(float x) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Value of lane ^ X (X = 8 or 4) within each 16-lane row, via DPP row rotation.
+template <int X>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
+    static_assert(X == 8 || X == 4, "row rotation");
+    if constexpr (X == 8) {
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xf, 0xf, false);  // row_ror:8
+    } else {
+        // lane ^ 4 within 8-lane halves.  row_ror:N makes lane l read lane (l - N) mod 16, so
+        // lanes with (l & 7) < 4 (source l + 4) take row_ror:12 and the others row_ror:4.
+        const uint32_t up = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x12c, 0xf, 0xf, false);
+        const uint32_t dn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xf, 0xf, false);
+        return ((threadIdx.x & 7) < 4) ? up : dn;
+    }
+}
+template <int X>
+__device__ __forceinline__ uint4 xor_lanes(uint4 v) {
+    return make_uint4(xor_lane<X>(v.x), xor_lane<X>(v.y), xor_lane<X>(v.z), xor_lane<X>(v.w));
+}
+
 template <int D, class BT>
 __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT b,
                                                                  const uint16_t* q, uint16_t* o,
@@ -397,7 +417,6 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
     // the current tile is computed
     struct Stage {
         uint4 k[NK];
-        uint4 kp[NK];  // rotate-half partner chunk of a new (not yet rotated) key row
         uint4 v[2];
     };
     Stage sa, sb;
@@ -406,7 +425,6 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
     auto gload = [&](int t, Stage& sg) {
         uint4* kreg = sg.k;
         uint4* vreg = sg.v;
-        uint4* kpart = sg.kp;
         const int kb = t * kTileKeys;
 #pragma unroll
         for (int it = 0; it < NK; ++it) {
@@ -416,7 +434,6 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
             if (j >= newbase && j < R) {
                 const uint16_t* src = k_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D;
                 kreg[it] = *reinterpret_cast<const uint4*>(src + col * 8);
-                kpart[it] = *reinterpret_cast<const uint4*>(src + ((col * 8) ^ (D / 2)));
             } else if (j < R) {
                 bool ik;
                 const int off = row_off(j, &ik);
@@ -452,6 +469,8 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
             const int row = c / CPR, col = c - row * CPR;
             const int j = kb + row;
             uint4 kv = kreg[it];
+            // the rotate-half partner chunk (dims +-D/2) of this row sits in lane ^ (CPR/2)
+            const uint4 pv = xor_lanes<CPR / 2>(kv);
             if (j >= newbase && j < R) {
                 // fused append: rotate this new key chunk, then also store it to its ring slot
                 const int d0 = col * 8;
@@ -460,7 +479,6 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
                 const float4* cs4 = reinterpret_cast<const float4*>(
                     st.rope + ((int64_t)d.s * st.max_step_rows + (j - newbase)) * (D / 2) + i0);
                 const uint32_t xw[4] = {kv.x, kv.y, kv.z, kv.w};
-                const uint4 pv = sg.kp[it];
                 const uint32_t yw[4] = {pv.x, pv.y, pv.z, pv.w};
                 uint32_t ow[4];
 #pragma unroll
@@ -515,7 +533,7 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
     for (int qg0 = 0; qg0 < M; qg0 += QPP) {
         const int mw = qg0 + QPW * w;
         const bool active = mw < M;
-        // the first tile's loads go out before the Q prologue so both latencies overlap
+        // the first tiles' loads go out before the Q prologue so both latencies overlap
         if (t0 < t1) gload(t0, sa);
         if (t0 + 1 < t1) gload(t0 + 1, sb);
 
@@ -846,6 +864,16 @@ __global__ __launch_bounds__(256) void evict_kernel(DevState st, BT b) {
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
+// One dispatch, through hipExtLaunchKernelGGL when the caller asks for timestamps.
+#define A2T_DISPATCH(kernel, grid, block, stream, kt, ...)                                        \
+    do {                                                                                          \
+        if ((kt).start)                                                                           \
+            hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, (kt).start, (kt).stop, 0,       \
+                                  __VA_ARGS__);                                                   \
+        else                                                                                      \
+            hipLaunchKernelGGL(kernel, grid, block, 0, stream, __VA_ARGS__);                      \
+    } while (0)
+
 // Calls f with the batch shrunk to the smallest of 1, 8 or kMaxDesc descriptors.
 template <template <int> class BT, class F>
 static hipError_t by_size(const BT<kMaxDesc>& b, F&& f) {
@@ -855,33 +883,35 @@ static hipError_t by_size(const BT<kMaxDesc>& b, F&& f) {
 }
 
 hipError_t launch_step_meta(const DevState& st, const StepBatch& b, const uint8_t* seg,
-                            const int32_t* pos, const int32_t* uid, hipStream_t stream) {
+                            const int32_t* pos, const int32_t* uid, hipStream_t stream,
+                            const KTimer& kt) {
     return by_size<StepBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
-        hipLaunchKernelGGL((step_meta_kernel<B>), dim3(b.max_n, b.count), dim3(64), 0, stream, st, bb,
+        A2T_DISPATCH((step_meta_kernel<B>), dim3(b.max_n, b.count), dim3(64), stream, kt, st, bb,
                            seg, pos, uid);
         return hipGetLastError();
     });
 }
 
 hipError_t launch_append(const DevState& st, const AppendBatch& b, int n_layers, const void* k,
-                         const void* v, hipStream_t stream) {
+                         const void* v, hipStream_t stream, const KTimer& kt) {
     const int cpr = st.Hkv * st.D / 8;
     const dim3 grid((b.max_n * cpr + 255) / 256, b.count, n_layers);
     return by_size<AppendBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
         if (st.dtype == 0)
-            hipLaunchKernelGGL((append_kernel<float, B>), grid, dim3(256), 0, stream, st, bb,
+            A2T_DISPATCH((append_kernel<float, B>), grid, dim3(256), stream, kt, st, bb,
                                static_cast<const float*>(k), static_cast<const float*>(v));
         else
-            hipLaunchKernelGGL((append_kernel<bf16_t, B>), grid, dim3(256), 0, stream, st, bb,
+            A2T_DISPATCH((append_kernel<bf16_t, B>), grid, dim3(256), stream, kt, st, bb,
                                static_cast<const bf16_t*>(k), static_cast<const bf16_t*>(v));
         return hipGetLastError();
     });
 }
 
 hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* q, void* o,
-                            const void* k_in, const void* v_in, hipStream_t stream) {
+                            const void* k_in, const void* v_in, hipStream_t stream,
+                            const KTimer& kt) {
     const uint16_t* ki = static_cast<const uint16_t*>(k_in);
     const uint16_t* vi = static_cast<const uint16_t*>(v_in);
     const dim3 grid(b.max_splits, st.Hkv, b.count);
@@ -890,10 +920,10 @@ hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* 
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
         if (st.D == 128)
-            hipLaunchKernelGGL((attn_mfma_kernel<128, B>), grid, dim3(kMfmaThreads), 0, stream, st, bb,
+            A2T_DISPATCH((attn_mfma_kernel<128, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
                                qq, oo, ki, vi);
         else if (st.D == 64)
-            hipLaunchKernelGGL((attn_mfma_kernel<64, B>), grid, dim3(kMfmaThreads), 0, stream, st, bb,
+            A2T_DISPATCH((attn_mfma_kernel<64, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
                                qq, oo, ki, vi);
         else
             return hipErrorInvalidValue;
@@ -903,60 +933,62 @@ hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* 
 
 template <typename T, int D, class B>
 static hipError_t valu_dispatch_g(const DevState& st, const B& b, const void* q, void* o,
-                                  hipStream_t stream) {
+                                  hipStream_t stream, const KTimer& kt) {
     const dim3 grid(b.max_splits, st.Hkv * b.max_rows, b.count);
     const T* qq = static_cast<const T*>(q);
     T* oo = static_cast<T*>(o);
     switch (st.Hq / st.Hkv) {
-        case 1: hipLaunchKernelGGL((attn_valu_kernel<T, D, 1, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
-        case 2: hipLaunchKernelGGL((attn_valu_kernel<T, D, 2, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
-        case 4: hipLaunchKernelGGL((attn_valu_kernel<T, D, 4, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
-        case 8: hipLaunchKernelGGL((attn_valu_kernel<T, D, 8, B>), grid, dim3(256), 0, stream, st, b, qq, oo); break;
+        case 1: A2T_DISPATCH((attn_valu_kernel<T, D, 1, B>), grid, dim3(256), stream, kt, st, b, qq, oo); break;
+        case 2: A2T_DISPATCH((attn_valu_kernel<T, D, 2, B>), grid, dim3(256), stream, kt, st, b, qq, oo); break;
+        case 4: A2T_DISPATCH((attn_valu_kernel<T, D, 4, B>), grid, dim3(256), stream, kt, st, b, qq, oo); break;
+        case 8: A2T_DISPATCH((attn_valu_kernel<T, D, 8, B>), grid, dim3(256), stream, kt, st, b, qq, oo); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_attn_valu(const DevState& st, const AttnBatch& b, const void* q, void* o,
-                            hipStream_t stream) {
+                            hipStream_t stream, const KTimer& kt) {
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
         if (st.dtype == 0) {
-            if (st.D == 128) return valu_dispatch_g<float, 128>(st, bb, q, o, stream);
-            if (st.D == 64) return valu_dispatch_g<float, 64>(st, bb, q, o, stream);
+            if (st.D == 128) return valu_dispatch_g<float, 128>(st, bb, q, o, stream, kt);
+            if (st.D == 64) return valu_dispatch_g<float, 64>(st, bb, q, o, stream, kt);
         } else {
-            if (st.D == 128) return valu_dispatch_g<bf16_t, 128>(st, bb, q, o, stream);
-            if (st.D == 64) return valu_dispatch_g<bf16_t, 64>(st, bb, q, o, stream);
+            if (st.D == 128) return valu_dispatch_g<bf16_t, 128>(st, bb, q, o, stream, kt);
+            if (st.D == 64) return valu_dispatch_g<bf16_t, 64>(st, bb, q, o, stream, kt);
         }
         (void)sizeof(B);
         return hipErrorInvalidValue;
     });
 }
 
-hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hipStream_t stream) {
+hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hipStream_t stream,
+                             const KTimer& kt) {
     const int G = st.Hq / st.Hkv;
     const int rpb = 256 / (st.D / 4);
     const dim3 grid((G * b.max_rows + rpb - 1) / rpb, st.Hkv, b.count);
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
         if (st.dtype == 0)
-            hipLaunchKernelGGL((attn_merge_kernel<float, B>), grid, dim3(256), 0, stream, st, bb,
+            A2T_DISPATCH((attn_merge_kernel<float, B>), grid, dim3(256), stream, kt, st, bb,
                                static_cast<float*>(o));
         else
-            hipLaunchKernelGGL((attn_merge_kernel<bf16_t, B>), grid, dim3(256), 0, stream, st, bb,
+            A2T_DISPATCH((attn_merge_kernel<bf16_t, B>), grid, dim3(256), stream, kt, st, bb,
                                static_cast<bf16_t*>(o));
         return hipGetLastError();
     });
 }
 
-hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream) {
+hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream,
+                        const KTimer& kt) {
     const dim3 grid(st.L + 1, b.count);
     return by_size<EvictBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
         if (st.dtype == 0)
-            hipLaunchKernelGGL((evict_kernel<4, B>), grid, dim3(256), 0, stream, st, bb);
+            A2T_DISPATCH((evict_kernel<4, B>), grid, dim3(256), stream, kt, st, bb);
         else
-            hipLaunchKernelGGL((evict_kernel<2, B>), grid, dim3(256), 0, stream, st, bb);
+            A2T_DISPATCH((evict_kernel<2, B>), grid, dim3(256), stream, kt, st, bb);
         return hipGetLastError();
     });
 }
