@@ -1,18 +1,30 @@
-"""Benchmark: the streaming KV unit step of a ten-minute session on one MI355X.
+"""Benchmark: the streaming KV unit step on one MI355X.
 
-One step = one listening unit of one stream through every layer: per layer
-an append (rotary keys into the cache) and causal chunk attention of the
-unit's rows over the resident cache, then budgeted eviction and compaction
-(36 layers, 32 query / 8 KV heads, head dim 128, bf16, budget 4096 rows,
-recent window 30 units).  The session runs from unit 0; the first --warmup
-units (the cache fills and eviction starts near unit 186) are untimed, the
-next --steps units are timed with HIP events on the cache's stream.
+Default workload (the headline line): a ten-minute single stream.  One step =
+one listening unit of one stream through every layer: per layer an append
+(rotary keys into the cache) and causal chunk attention of the unit's rows
+over the resident cache, then budgeted eviction and compaction (36 layers,
+32 query / 8 KV heads, head dim 128, bf16, budget 4096 rows, recent window
+30 units).  The session runs from unit 0; the first --warmup units (the cache
+fills and eviction starts near unit 186) are untimed, the next --steps units
+are timed with HIP events on the cache's stream.
+
+--workload varlen: 32 streams of 60..600 units with random start steps and
+budgets of 2048 or 4096 rows, all active streams of a global step batched in
+one call per layer (rate = stream unit-steps/s).
+
+--workload decode: 64 streams filled with 600 listening units each, then
+single-row response decode steps, all streams batched (rate = stream
+decode-steps/s).
 
 Inputs are synthetic and seeded (synth/): stream structure exactly as the
-workload defines it; Q/K/V values cycle through a pool of pre-generated unit
-tensors already resident in HBM (values do not change the work done).
+workload defines it; Q/K/V values come from a pool of pre-generated tensors
+already resident in HBM (values do not change the work done).
 
-Prints one JSON line.  See the design doc for the byte accounting.
+Prints one JSON line with the rate, the dominant kernel's roofline (its
+average dispatch time from kernel-accurate HIP event timestamps over extra
+profiled steps, against the algorithmic bytes per launch) and, for the
+default workload, the float64 CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -33,13 +45,27 @@ if ROOT not in sys.path:
 from synth.streams import CONFIGS, make_workload, step_values  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
-METRIC = "stream unit-steps/s (append+attn+evict) and achieved HBM GB/s vs peak"
 POOL = 8
+KEEP_SEGS = (0, 3, 4)     # PREFIX, TEXT, RESPONSE: never evicted
+
+METRICS = {
+    "stream": ("stream unit-steps/s (append+attn+evict) and achieved HBM GB/s vs peak",
+               "unit-steps/s"),
+    "varlen": ("stream unit-steps/s (append+attn+evict), varlen batch of 32 streams",
+               "unit-steps/s"),
+    "decode": ("stream decode-steps/s (append+decode attn+evict), batch of 64 streams",
+               "decode-steps/s"),
+}
+DEFAULTS = {  # warmup, steps, profile steps
+    "stream": (200, 400, 100),
+    "varlen": (100, 400, 100),
+    "decode": (20, 150, 30),
+}
 
 
 def attn_bytes(R: int, n_q: int, cfg) -> int:
-    """Algorithmic HBM bytes of one chunk-attention launch for one stream-layer:
-    every resident K and V row read once, Q read once, O written once."""
+    """Algorithmic HBM bytes of one stream-layer of attention: every resident
+    K and V row read once, Q read once, O written once."""
     elt = 2 if cfg.dtype == "bf16" else 4
     kv = R * 2 * cfg.n_kv_heads * cfg.head_dim * elt
     qo = 2 * n_q * cfg.n_q_heads * cfg.head_dim * elt
@@ -47,13 +73,22 @@ def attn_bytes(R: int, n_q: int, cfg) -> int:
 
 
 def step_bytes(R_attn: int, n: int, n_moved: int, R_pre: int, cfg) -> int:
-    """Algorithmic HBM bytes of one unit step over all layers: attention reads,
-    the append (read the staged K/V, write the rows), the kept rows copied by
-    compaction (read + write), and the per-row metadata the eviction scans."""
+    """Algorithmic HBM bytes of one stream step over all layers: attention
+    reads, the append (read the staged K/V, write the rows), the kept rows
+    copied by compaction (read + write), and the per-row metadata the
+    eviction scans."""
     elt = 2 if cfg.dtype == "bf16" else 4
     row = 2 * cfg.n_kv_heads * cfg.head_dim * elt
     per_layer = attn_bytes(R_attn, n, cfg) + 2 * n * row + 2 * n_moved * row
     return cfg.n_layers * per_layer + 9 * R_pre
+
+
+def _threads_used() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return int(max([p.get("num_threads", 1) for p in threadpool_info()] + [1]))
+    except Exception:  # pragma: no cover
+        return os.cpu_count() or 1
 
 
 def cpu_baseline(cfg, spec, seed, start_unit, sample_units, sample_layers):
@@ -63,7 +98,7 @@ def cpu_baseline(cfg, spec, seed, start_unit, sample_units, sample_layers):
     from oracle.replay import resume
     layers = list(range(sample_layers))
     cache = resume(cfg, seed, spec, cfg.budget, cfg.window, start_unit, layers)
-    vals = [step_values(cfg, seed, 0, spec.steps[u].key, spec.steps[u].n, layers)
+    vals = [step_values(cfg, seed, spec.stream, spec.steps[u].key, spec.steps[u].n, layers)
             for u in range(start_unit, start_unit + sample_units)]
     t0 = time.perf_counter()
     for j, u in enumerate(range(start_unit, start_unit + sample_units)):
@@ -73,78 +108,130 @@ def cpu_baseline(cfg, spec, seed, start_unit, sample_units, sample_layers):
                      {l: v["v"][i] for i, l in enumerate(layers)})
         for i, l in enumerate(layers):
             cache.attention(l, v["q"][i])
-        cache.evict(cfg.budget, cfg.window)
+        cache.evict(spec.budget, cfg.window)
     dt = time.perf_counter() - t0
     per_unit_all_layers = dt / sample_units * (cfg.n_layers / sample_layers)
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
-    return {"value": 1.0 / per_unit_all_layers, "unit": "unit-steps/s", "cores": int(cores),
+    return {"value": 1.0 / per_unit_all_layers, "unit": "unit-steps/s", "cores": _threads_used(),
             "kind": "oracle",
             "sample": f"{sample_units} steady-state units (from unit {start_unit}) x "
                       f"{sample_layers} of {cfg.n_layers} layers, fp64 numpy, scaled to "
                       f"{cfg.n_layers} layers; {dt:.1f} s of CPU work"}
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=400)
-    ap.add_argument("--warmup", type=int, default=200)
-    ap.add_argument("--seed", type=int, default=1)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-units", type=int, default=6)
-    ap.add_argument("--cpu-sample-layers", type=int, default=4)
-    ap.add_argument("--profile-steps", type=int, default=100,
-                    help="extra timed units with per-kernel HIP events (roofline)")
-    ap.add_argument("--unfused", action="store_true",
-                    help="per layer a2t_append then a2t_chunk_attn (default: a2t_append_attn)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(the KV step shards by stream or KV head with no exchange; see DESIGN.md).",
-              file=sys.stderr)
-        sys.exit(2)
+class Runner:
+    """Shared plumbing: the library, a cache on torch's current stream, and
+    per-kernel dispatch timing."""
 
-    import torch
-    import paper_2609_31224_amd as a2t
+    KERNELS = ("attn_mfma", "attn_valu", "attn_merge", "append", "step_meta", "evict")
 
+    def __init__(self, cfg, n_streams, unit_rows, kept_rows, max_n):
+        import torch
+        import paper_2609_31224_amd as a2t
+        self.torch, self.a2t, self.cfg = torch, a2t, cfg
+        self.dev = torch.device("cuda:0")
+        torch.cuda.set_device(self.dev)
+        self.stream = torch.cuda.current_stream()
+        self.cache = a2t.a2t_cache_create(cfg.n_layers, n_streams, cfg.n_q_heads, cfg.n_kv_heads,
+                                          cfg.head_dim, a2t.A2T_BF16, unit_rows, kept_rows, max_n,
+                                          rope_theta=cfg.rope_theta, attn_scale=cfg.scale,
+                                          stream=self.stream)
+        self.lib = a2t.raw_lib()
+        self.h = self.cache.ptr
+        self.info = a2t.a2t_stream_info()
+
+    def check(self, rc, name):
+        if rc:
+            raise self.a2t.A2TError(rc, name)
+
+    def stream_info(self, s):
+        self.lib.a2t_stream_info_get(self.h, s, C.byref(self.info))
+        return self.info
+
+    def pool(self, shape, seed):
+        """bf16 N(0,1) values from a seeded device generator (timing inputs)."""
+        g = self.torch.Generator(device=self.dev)
+        g.manual_seed(seed)
+        return self.torch.randn(shape, generator=g, device=self.dev,
+                                dtype=self.torch.float32).to(self.torch.bfloat16)
+
+    def timed(self, fn, steps):
+        """Run fn(j) for j < steps with an event at every step boundary."""
+        torch = self.torch
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        evs[0].record(self.stream)
+        for j in range(steps):
+            fn(j)
+            evs[j + 1].record(self.stream)
+        t_enqueue = time.perf_counter() - t_wall
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter() - t_wall
+        step_ms = np.array([evs[j].elapsed_time(evs[j + 1]) for j in range(steps)])
+        total_ms = float(evs[0].elapsed_time(evs[-1]))
+        return step_ms, total_ms, t_wall, t_enqueue
+
+    def profiled(self, fn, steps):
+        """Run fn(j) with every dispatch timestamped; per-kernel averages."""
+        self.a2t.a2t_profile_enable(self.cache, "")
+        for j in range(steps):
+            fn(j)
+        self.torch.cuda.synchronize()
+        kern = {}
+        for name in self.KERNELS:
+            n_launch, ms = self.a2t.a2t_kernel_time(self.cache, name)
+            if n_launch:
+                kern[name] = {"launches": n_launch, "avg_us": ms * 1e3 / n_launch}
+        self.a2t.a2t_profile_enable(self.cache, None)
+        return kern
+
+    def close(self):
+        self.a2t.a2t_cache_destroy(self.cache)
+
+
+def roofline(kernel, kern, alg_bytes):
+    us = kern.get(kernel, {}).get("avg_us")
+    achieved = alg_bytes / (us * 1e-6) / 1e9 if us else None
+    return {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS if achieved else None,
+            "traffic": None, "avg_launch_us": us, "alg_bytes_per_launch": alg_bytes}
+
+
+def timing_fields(step_ms, total_ms, steps, t_wall, t_enqueue):
+    return {"unit_ms": {"mean": float(step_ms.mean()), "p50": float(np.percentile(step_ms, 50)),
+                        "p99": float(np.percentile(step_ms, 99)), "max": float(step_ms.max()),
+                        "over_1s": int((step_ms > 1000).sum())},
+            "host_wall_s": t_wall, "host_enqueue_ms_per_step": t_enqueue * 1e3 / steps}
+
+
+# ------------------------------------------------------------ ten-minute stream
+def run_stream(args):
     base = CONFIGS[1]
     total_units = args.warmup + args.steps + args.profile_steps
     cfg = dataclasses.replace(base, units=max(base.units, total_units))
     spec = make_workload(cfg, seed=args.seed, units=total_units).streams[0]
     L, Hq, Hkv, D = cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     max_n = cfg.max_unit_rows
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    stream = torch.cuda.current_stream()
+    keep_rows = sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in spec.steps)
+    unit_rows = max(cfg.budget, cfg.window * max_n) + 2 * max_n
+    r = Runner(cfg, 1, unit_rows, keep_rows + 64, max_n)
+    torch, lib, h = r.torch, r.lib, r.h
 
     # value pool: POOL unit tensors of the largest unit size, all layers, in HBM
-    qp = torch.empty(POOL, L, max_n, Hq, D, dtype=torch.bfloat16, device=dev)
-    kp = torch.empty(POOL, L, max_n, Hkv, D, dtype=torch.bfloat16, device=dev)
-    vp = torch.empty(POOL, L, max_n, Hkv, D, dtype=torch.bfloat16, device=dev)
+    qp = torch.empty(POOL, L, max_n, Hq, D, dtype=torch.bfloat16, device=r.dev)
+    kp = torch.empty(POOL, L, max_n, Hkv, D, dtype=torch.bfloat16, device=r.dev)
+    vp = torch.empty(POOL, L, max_n, Hkv, D, dtype=torch.bfloat16, device=r.dev)
     for p in range(POOL):
         vals = step_values(cfg, args.seed, 0, 1_000_000 + p, max_n, range(L))
         qp[p] = torch.from_numpy(vals["q"]).to(torch.bfloat16)
         kp[p] = torch.from_numpy(vals["k"]).to(torch.bfloat16)
         vp[p] = torch.from_numpy(vals["v"]).to(torch.bfloat16)
-    out = torch.empty(max_n, Hq, D, dtype=torch.bfloat16, device=dev)
+    out = torch.empty(max_n, Hq, D, dtype=torch.bfloat16, device=r.dev)
 
-    keep_rows = sum(int(np.isin(st.seg, (0, 3, 4)).sum()) for st in spec.steps)
-    unit_rows = max(cfg.budget, cfg.window * max_n) + 2 * max_n
-    cache = a2t.a2t_cache_create(L, 1, Hq, Hkv, D, a2t.A2T_BF16, unit_rows, keep_rows + 64, max_n,
-                                 rope_theta=cfg.rope_theta, attn_scale=cfg.scale, stream=stream)
-    lib = a2t.raw_lib()
-    h = cache.ptr
     ids = (C.c_int32 * 1)(0)
     budget = (C.c_int32 * 1)(cfg.budget)
     n_ev = (C.c_int32 * 1)()
     unmet = (C.c_uint8 * 1)()
-    info = a2t.a2t_stream_info()
-
-    # per-unit marshalled metadata
     metas = []
     for st in spec.steps:
         n = st.n
@@ -164,79 +251,41 @@ def main():
             off_kv = (p * L + layer) * row_stride_kv
             meta = (seg, pos, unit) if layer == 0 else (None, None, None)
             if args.unfused:
-                rc = lib.a2t_append(h, layer, 1, ids, nrows, k_base + off_kv, v_base + off_kv, *meta)
-                if rc:
-                    raise a2t.A2TError(rc, "a2t_append")
-                rc = lib.a2t_chunk_attn(h, layer, 1, ids, nrows, q_base + off_q, o_ptr)
-                if rc:
-                    raise a2t.A2TError(rc, "a2t_chunk_attn")
+                r.check(lib.a2t_append(h, layer, 1, ids, nrows, k_base + off_kv, v_base + off_kv,
+                                       *meta), "a2t_append")
+                r.check(lib.a2t_chunk_attn(h, layer, 1, ids, nrows, q_base + off_q, o_ptr),
+                        "a2t_chunk_attn")
             else:
-                rc = lib.a2t_append_attn(h, layer, 1, ids, nrows, k_base + off_kv, v_base + off_kv,
-                                         *meta, nrows, q_base + off_q, o_ptr)
-                if rc:
-                    raise a2t.A2TError(rc, "a2t_append_attn")
+                r.check(lib.a2t_append_attn(h, layer, 1, ids, nrows, k_base + off_kv,
+                                            v_base + off_kv, *meta, nrows, q_base + off_q, o_ptr),
+                        "a2t_append_attn")
         if record:
-            lib.a2t_stream_info_get(h, 0, C.byref(info))
-            R_attn = info.resident
-        rc = lib.a2t_evict(h, 1, ids, budget, cfg.window, n_ev, unmet)
-        if rc:
-            raise a2t.A2TError(rc, "a2t_evict")
+            R_attn = r.stream_info(0).resident
+        r.check(lib.a2t_evict(h, 1, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
         if record:
-            lib.a2t_stream_info_get(h, 0, C.byref(info))
-            R_log.append((R_attn, nrows[0], int(n_ev[0]), info.moved_total))
+            R_log.append((R_attn, nrows[0], int(n_ev[0]), r.stream_info(0).moved_total))
 
     for u in range(args.warmup):
         run_unit(u)
-    torch.cuda.synchronize()
-
-    # ---- timed region: K unit steps, an event at every unit boundary
-    lib.a2t_stream_info_get(h, 0, C.byref(info))
-    moved_before = info.moved_total
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    evs[0].record(stream)
-    for j in range(args.steps):
-        run_unit(args.warmup + j, record=True)
-        evs[j + 1].record(stream)
-    t_enqueue = time.perf_counter() - t_wall
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    unit_ms = np.array([evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps)])
-    total_ms = float(evs[0].elapsed_time(evs[-1]))
+    moved_before = r.stream_info(0).moved_total
+    step_ms, total_ms, t_wall, t_enq = r.timed(
+        lambda j: run_unit(args.warmup + j, record=True), args.steps)
     ms_per_step = total_ms / args.steps
 
     # algorithmic bytes of the timed steps
-    moved_prev = moved_before
-    tot_bytes = 0
-    attn_alg = []
-    for (R_attn, n, ev, moved_total) in R_log:
-        moved = moved_total - moved_prev
+    moved_prev, tot_bytes = moved_before, 0
+    for (R_attn, n, _, moved_total) in R_log:
+        tot_bytes += step_bytes(R_attn, n, moved_total - moved_prev, R_attn, cfg)
         moved_prev = moved_total
-        tot_bytes += step_bytes(R_attn, n, moved, R_attn, cfg)
-        attn_alg.append(attn_bytes(R_attn, n, cfg))
     step_gbps = tot_bytes / (total_ms * 1e-3) / 1e9
 
-    # ---- per-kernel timing pass (same stream, HIP events around each launch)
-    kern = {}
-    prof_units = range(args.warmup + args.steps, args.warmup + args.steps + args.profile_steps)
-    a2t.a2t_profile_enable(cache, "")
     R_log.clear()
-    for u in prof_units:
-        run_unit(u, record=True)
-    torch.cuda.synchronize()
-    for name in ("attn_mfma", "attn_merge", "append", "step_meta", "evict"):
-        n_launch, ms = a2t.a2t_kernel_time(cache, name)
-        kern[name] = {"launches": n_launch, "avg_us": (ms * 1e3 / n_launch) if n_launch else None}
-    a2t.a2t_profile_enable(cache, None)
-    prof_attn_bytes = np.mean([attn_bytes(R, n, cfg) for (R, n, _, _) in R_log]) if R_log else 0.0
-    attn_us = kern["attn_mfma"]["avg_us"]
-    achieved = prof_attn_bytes / (attn_us * 1e-6) / 1e9 if attn_us else None
-
-    lib.a2t_stream_info_get(h, 0, C.byref(info))
-    peak = info.peak
+    p0 = args.warmup + args.steps
+    kern = r.profiled(lambda j: run_unit(p0 + j, record=True), args.profile_steps)
+    prof_attn_bytes = float(np.mean([attn_bytes(R, n, cfg) for (R, n, _, _) in R_log]))
+    peak = r.stream_info(0).peak
     rows_no_evict = spec.total_rows()
-    a2t.a2t_cache_destroy(cache)
+    r.close()
 
     base_line = None
     if not args.no_cpu_baseline:
@@ -244,20 +293,9 @@ def main():
         base_spec = make_workload(base, seed=args.seed).streams[0]
         base_line = cpu_baseline(base, base_spec, args.seed, start, args.cpu_sample_units,
                                  args.cpu_sample_layers)
-
-    result = {
-        "metric": METRIC,
+    res = {
         "value": 1000.0 / ms_per_step,
-        "unit": "unit-steps/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
         "config": {
             "workload": "ten-minute single stream: 36 layers, 32 query / 8 KV heads, head dim 128, "
                         "bf16, units of 17 acoustic + 2 delimiter + Poisson(3) transcript rows, "
@@ -267,30 +305,260 @@ def main():
                      else "a2t_append_attn per layer",
             "seed": args.seed,
         },
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "attn_mfma",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS if achieved else None,
-            "traffic": None,
-            "avg_launch_us": attn_us,
-            "alg_bytes_per_launch": prof_attn_bytes,
-        },
+        "roofline": roofline("attn_mfma", kern, prof_attn_bytes),
         "step_hbm": {"achieved_gbps": step_gbps, "frac": step_gbps / HBM_PEAK_GBPS,
                      "alg_bytes_per_step": tot_bytes / max(1, args.steps)},
-        "unit_ms": {"mean": float(unit_ms.mean()), "p50": float(np.percentile(unit_ms, 50)),
-                    "p99": float(np.percentile(unit_ms, 99)), "max": float(unit_ms.max()),
-                    "over_1s": int((unit_ms > 1000).sum())},
+        **timing_fields(step_ms, total_ms, args.steps, t_wall, t_enq),
         "kernels_us": kern,
         "peak_rows": peak,
         "rows_without_eviction": rows_no_evict,
         "peak_reduction": 1.0 - peak / rows_no_evict,
-        "host_wall_s": t_wall,
-        "host_enqueue_ms_per_step": t_enqueue * 1e3 / args.steps,
         "cpu_baseline": base_line,
     }
+    return res
+
+
+# ------------------------------------------------------------------- varlen batch
+def run_varlen(args):
+    cfg = CONFIGS[2]
+    w = make_workload(cfg, seed=args.seed)
+    specs = w.streams
+    S, L, Hq, Hkv, D = len(specs), cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    T = w.global_steps()
+    max_n = cfg.max_unit_rows
+    keep_rows = max(sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in s.steps) for s in specs)
+    unit_rows = max(max(s.budget for s in specs), cfg.window * max_n) + 2 * max_n
+    r = Runner(cfg, S, unit_rows, keep_rows + 64, max_n)
+    torch, lib, h = r.torch, r.lib, r.h
+
+    # per global step: the active streams and their marshalled metadata
+    steps = []
+    for t in range(T):
+        act = [(i, s.steps[t - s.offset]) for i, s in enumerate(specs)
+               if 0 <= t - s.offset < len(s.steps)]
+        if not act:
+            steps.append(None)
+            continue
+        n = len(act)
+        seg = np.concatenate([st.seg for _, st in act])
+        pos = np.concatenate([st.pos for _, st in act])
+        steps.append(dict(
+            n=n, rows=[st.n for _, st in act], ids=(C.c_int32 * n)(*[i for i, _ in act]),
+            nrows=(C.c_int32 * n)(*[st.n for _, st in act]),
+            seg=(C.c_uint8 * len(seg))(*seg.tolist()), pos=(C.c_int32 * len(pos))(*pos.tolist()),
+            unit=(C.c_int32 * n)(*[st.unit for _, st in act]),
+            budget=(C.c_int32 * n)(*[specs[i].budget for i, _ in act]),
+            n_ev=(C.c_int32 * n)(), unmet=(C.c_uint8 * n)()))
+    max_rows = max(sum(s["rows"]) for s in steps if s)
+    P = 2
+    qp = r.pool((P, L, max_rows, Hq, D), args.seed)
+    kp = r.pool((P, L, max_rows, Hkv, D), args.seed + 1)
+    vp = r.pool((P, L, max_rows, Hkv, D), args.seed + 2)
+    out = torch.empty(max_rows, Hq, D, dtype=torch.bfloat16, device=r.dev)
+    sq, skv = max_rows * Hq * D * 2, max_rows * Hkv * D * 2
+    R_log = []
+
+    def run_step(t, record=False):
+        st = steps[t]
+        if st is None:
+            return
+        p = t % P
+        for layer in range(L):
+            oq, okv = (p * L + layer) * sq, (p * L + layer) * skv
+            meta = (st["seg"], st["pos"], st["unit"]) if layer == 0 else (None, None, None)
+            r.check(lib.a2t_append_attn(h, layer, st["n"], st["ids"], st["nrows"],
+                                        kp.data_ptr() + okv, vp.data_ptr() + okv, *meta,
+                                        st["nrows"], qp.data_ptr() + oq, out.data_ptr()),
+                    "a2t_append_attn")
+        if record:
+            R_log.append(sum(attn_bytes(r.stream_info(i).resident, n, cfg)
+                             for i, n in zip(st["ids"], st["rows"])))
+        r.check(lib.a2t_evict(h, st["n"], st["ids"], st["budget"], cfg.window, st["n_ev"],
+                              st["unmet"]), "a2t_evict")
+
+    warm = min(args.warmup, T)
+    timed_steps = max(0, min(args.steps, T - warm))
+    prof_steps = max(0, min(args.profile_steps, T - warm - timed_steps))
+    for t in range(warm):
+        run_step(t)
+    step_ms, total_ms, t_wall, t_enq = r.timed(lambda j: run_step(warm + j), timed_steps)
+    stream_steps = sum(steps[t]["n"] for t in range(warm, warm + timed_steps) if steps[t])
+    p0 = warm + timed_steps
+    kern = r.profiled(lambda j: run_step(p0 + j, record=True), prof_steps)
+    # one attention launch per layer covers every active stream of the step
+    alg = float(np.mean(R_log)) if R_log else 0.0
+    unmet_streams = sum(1 for i in range(S) if r.stream_info(i).budget_unmet)
+    r.close()
+    return {
+        "value": stream_steps / (total_ms * 1e-3),
+        "ms_per_step": total_ms / max(1, timed_steps),
+        "config": {
+            "workload": "varlen batch: 32 streams of U{60..600} units at random start steps in "
+                        "a 600-step schedule, budgets {2048, 4096} rows, recent window 30 units; "
+                        "36 layers, 32 query / 8 KV heads, head dim 128, bf16",
+            "timed_global_steps": [warm, warm + timed_steps],
+            "stream_steps_timed": stream_steps,
+            "mean_active_streams": stream_steps / max(1, timed_steps),
+            "calls": "a2t_append_attn per layer over all active streams, one a2t_evict per step",
+            "seed": args.seed,
+        },
+        "roofline": roofline("attn_mfma", kern, alg),
+        **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
+        "kernels_us": kern,
+        "streams_budget_unmet_at_end": unmet_streams,
+        "cpu_baseline": None,
+    }
+
+
+# ------------------------------------------------------------------- decode batch
+def run_decode(args):
+    cfg = CONFIGS[3]
+    w = make_workload(cfg, seed=args.seed)
+    specs = w.streams
+    S, L, Hq, Hkv, D = len(specs), cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    n_units = specs[0].n_units
+    n_dec = len(specs[0].steps) - n_units
+    max_n = cfg.max_unit_rows
+    keep_rows = max(sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in s.steps) for s in specs)
+    unit_rows = max(cfg.budget, cfg.window * max_n) + 2 * max_n + n_dec
+    r = Runner(cfg, S, unit_rows, keep_rows + 64, max_n)
+    torch, lib, h = r.torch, r.lib, r.h
+    ids = (C.c_int32 * S)(*range(S))
+    budget = (C.c_int32 * S)(*[cfg.budget] * S)
+    n_ev, unmet = (C.c_int32 * S)(), (C.c_uint8 * S)()
+
+    # fill: every listening unit of every stream, all layers in one append call
+    fill_rows = max(sum(s.steps[u].n for s in specs) for u in range(n_units))
+    kf = r.pool((L, fill_rows, Hkv, D), args.seed + 10)
+    vf = r.pool((L, fill_rows, Hkv, D), args.seed + 11)
+    for u in range(n_units):
+        seg = np.concatenate([s.steps[u].seg for s in specs])
+        pos = np.concatenate([s.steps[u].pos for s in specs])
+        nrows = (C.c_int32 * S)(*[s.steps[u].n for s in specs])
+        unit = (C.c_int32 * S)(*[s.steps[u].unit for s in specs])
+        # the all-layers input is packed [L][sum n][Hkv][D]: re-pack for this unit's row count
+        tot = int(sum(nrows))
+        kk = kf[:, :tot].contiguous() if tot < fill_rows else kf
+        vv = vf[:, :tot].contiguous() if tot < fill_rows else vf
+        r.check(lib.a2t_append(h, -1, S, ids, nrows, kk.data_ptr(), vv.data_ptr(),
+                               (C.c_uint8 * tot)(*seg.tolist()), (C.c_int32 * tot)(*pos.tolist()),
+                               unit), "a2t_append")
+        r.check(lib.a2t_evict(h, S, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
+    torch.cuda.synchronize()
+
+    # decode steps: one RESPONSE row per stream
+    dmeta = []
+    for d in range(n_dec):
+        st = [s.steps[n_units + d] for s in specs]
+        dmeta.append(((C.c_uint8 * S)(*[int(x.seg[0]) for x in st]),
+                      (C.c_int32 * S)(*[int(x.pos[0]) for x in st]),
+                      (C.c_int32 * S)(*[x.unit for x in st])))
+    ones = (C.c_int32 * S)(*[1] * S)
+    P = 4
+    qp = r.pool((P, L, S, Hq, D), args.seed)
+    kp = r.pool((P, L, S, Hkv, D), args.seed + 1)
+    vp = r.pool((P, L, S, Hkv, D), args.seed + 2)
+    out = torch.empty(S, Hq, D, dtype=torch.bfloat16, device=r.dev)
+    sq, skv = S * Hq * D * 2, S * Hkv * D * 2
+    fused = args.decode_call == "fused"
+    R_log = []
+
+    def run_step(d, record=False):
+        seg, pos, unit = dmeta[d]
+        p = d % P
+        for layer in range(L):
+            oq, okv = (p * L + layer) * sq, (p * L + layer) * skv
+            meta = (seg, pos, unit) if layer == 0 else (None, None, None)
+            if fused:
+                r.check(lib.a2t_append_attn(h, layer, S, ids, ones, kp.data_ptr() + okv,
+                                            vp.data_ptr() + okv, *meta, ones, qp.data_ptr() + oq,
+                                            out.data_ptr()), "a2t_append_attn")
+            else:
+                r.check(lib.a2t_append(h, layer, S, ids, ones, kp.data_ptr() + okv,
+                                       vp.data_ptr() + okv, *meta), "a2t_append")
+                r.check(lib.a2t_decode_attn(h, layer, S, ids, qp.data_ptr() + oq, out.data_ptr()),
+                        "a2t_decode_attn")
+        if record:
+            R_log.append(sum(attn_bytes(r.stream_info(i).resident, 1, cfg) for i in range(S)))
+        r.check(lib.a2t_evict(h, S, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
+
+    warm = min(args.warmup, n_dec)
+    timed_steps = max(0, min(args.steps, n_dec - warm))
+    prof_steps = max(0, min(args.profile_steps, n_dec - warm - timed_steps))
+    for d in range(warm):
+        run_step(d)
+    step_ms, total_ms, t_wall, t_enq = r.timed(lambda j: run_step(warm + j), timed_steps)
+    p0 = warm + timed_steps
+    kern = r.profiled(lambda j: run_step(p0 + j, record=True), prof_steps)
+    alg = float(np.mean(R_log)) if R_log else 0.0
+    mean_R = float(np.mean([r.stream_info(i).resident for i in range(S)]))
+    r.close()
+    kname = "attn_mfma" if fused else "attn_valu"
+    return {
+        "value": S * timed_steps / (total_ms * 1e-3),
+        "ms_per_step": total_ms / max(1, timed_steps),
+        "config": {
+            "workload": "decode batch: 64 streams, each filled with 600 listening units "
+                        "(budget 4096 rows, recent window 30 units), then single-row response "
+                        "decode steps; 36 layers, 32 query / 8 KV heads, head dim 128, bf16",
+            "timed_decode_steps": [warm, warm + timed_steps],
+            "calls": ("a2t_append_attn (n_q = 1)" if fused else "a2t_append + a2t_decode_attn")
+                     + " per layer over 64 streams, one a2t_evict per step",
+            "mean_resident_rows_at_end": mean_R,
+            "seed": args.seed,
+        },
+        "roofline": roofline(kname, kern, alg),
+        **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
+        "kernels_us": kern,
+        "cpu_baseline": None,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--workload", choices=sorted(METRICS), default="stream")
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--profile-steps", type=int, default=None,
+                    help="extra steps with every dispatch timestamped (roofline)")
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-units", type=int, default=6)
+    ap.add_argument("--cpu-sample-layers", type=int, default=4)
+    ap.add_argument("--unfused", action="store_true",
+                    help="stream workload: per layer a2t_append then a2t_chunk_attn")
+    ap.add_argument("--decode-call", choices=("decode", "fused"), default="decode",
+                    help="decode workload: a2t_append + a2t_decode_attn, or a2t_append_attn")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the KV step shards by stream or by KV head with no exchange).", file=sys.stderr)
+        sys.exit(2)
+    w, s, p = DEFAULTS[args.workload]
+    args.warmup = w if args.warmup is None else args.warmup
+    args.steps = s if args.steps is None else args.steps
+    args.profile_steps = p if args.profile_steps is None else args.profile_steps
+    if args.seed is None:
+        args.seed = {"stream": 1, "varlen": 2, "decode": 3}[args.workload]
+
+    res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode}[args.workload](args)
+    metric, unit = METRICS[args.workload]
+    result = {
+        "metric": metric,
+        "value": res.pop("value"),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res.pop("ms_per_step"),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+    }
+    result.update(res)
     print(json.dumps(result), flush=True)
 
 

@@ -236,8 +236,7 @@ int choose_splits(const a2t_cache* c, int n_desc, int max_R, int64_t floats_per_
 // With in_row0 non-null (bf16 MFMA path only) the launch also appends each
 // stream's open-step rows of `layer` from k_in / v_in.
 int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_t* n_q,
-                const int32_t* q_row0, const void* q, void* o, bool decode,
-                const int32_t* in_row0 = nullptr, const void* k_in = nullptr,
+                const int32_t* q_row0, const void* q, void* o, const int32_t* in_row0 = nullptr, const void* k_in = nullptr,
                 const void* v_in = nullptr) {
     AttnBatch b{};
     b.count = n;
@@ -272,7 +271,10 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     }
     b.max_splits = splits;
     b.max_rows = max_rows;
-    const bool valu = decode || c->cfg.dtype == A2T_F32 || c->force_valu;
+    // bf16 caches use the MFMA kernel for decode too: with one query row per
+    // stream it is still bound by streaming the resident K/V, and its staged
+    // tile pipeline keeps more bytes in flight than the VALU kernel.
+    const bool valu = c->cfg.dtype == A2T_F32 || c->force_valu;
     hipError_t e;
     {
         ProfScope ps(c, valu ? "attn_valu" : "attn_mfma");
@@ -311,7 +313,7 @@ int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* i
     DeviceGuard dg(c->cfg.device);
     for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
         const int n = std::min(kMaxDesc, n_streams - i0);
-        rc = attn_launch(c, layer, n, ids + i0, nq.data() + i0, row0.data() + i0, q, o, decode);
+        rc = attn_launch(c, layer, n, ids + i0, nq.data() + i0, row0.data() + i0, q, o);
         if (rc) return rc;
     }
     return A2T_OK;
@@ -680,8 +682,8 @@ int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_
     }
     for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
         const int n = std::min(kMaxDesc, n_streams - i0);
-        rc = attn_launch(c, layer, n, ids + i0, n_q + i0, row0.data() + i0, q, o, false,
-                         in0.data() + i0, kin, vin);
+        rc = attn_launch(c, layer, n, ids + i0, n_q + i0, row0.data() + i0, q, o, in0.data() + i0,
+                         kin, vin);
         if (rc) return rc;
     }
     return A2T_OK;

@@ -8,9 +8,10 @@
 //               positions; they are never re-encoded later).
 //   attn_mfma   causal chunk attention of a step's new rows over the resident
 //               cache, bf16 MFMA 16x16x32 for Q.K^T and P.V, online softmax
-//               with wave shuffles, key splits for parallelism.
+//               with wave shuffles, key splits for parallelism; also bf16
+//               decode (one query row per stream).
 //   attn_valu   the same attention on the vector ALU, one query row per
-//               workgroup column: fp32 caches and single-row decode.
+//               workgroup column: fp32 caches (chunk and decode).
 //   attn_merge  combines key-split partials (fixed order, deterministic).
 //   evict       eviction and compaction (Sec. 3.3): a ballot/prefix-sum scan
 //               over the passed-over ring rows keeps TEXT/RESPONSE/PREFIX rows

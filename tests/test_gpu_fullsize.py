@@ -1,0 +1,68 @@
+"""GPU parity at full workload sizes, in the benchmark's batched call pattern.
+
+The batched varlen listening workload (32 streams, 600-step schedule) and the
+speaking-phase decode workload (64 streams, 600-unit fill, 200 decode steps)
+run whole.  Eviction counts, budget flags, final layouts and peaks are checked
+for every stream against the oracle's policy replay; attention and stored
+K/V on sampled streams and layers against the fp64 oracle (bf16 bar 2e-2).
+"""
+import numpy as np
+import pytest
+
+from synth.streams import CONFIGS, make_workload
+from tests.fullsize import SampledBatch
+from tests.harness import row_bounds
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+KEEP = (0, 3, 4)
+
+
+def _caps(cfg, specs, extra=0):
+    max_n = cfg.max_unit_rows
+    unit_rows = max(max(s.budget for s in specs), cfg.window * max_n) + 2 * max_n + extra
+    kept = max(row_bounds(s)[1] for s in specs) + 64
+    return unit_rows, kept, max_n
+
+
+def test_config2_full_varlen_batched(gpu):
+    cfg = CONFIGS[2]
+    specs = make_workload(cfg).streams
+    # sample the longest stream of each budget: both evict, the 2048 one past its floor
+    sampled = []
+    for b in cfg.budget_choices:
+        cand = [i for i, s in enumerate(specs) if s.budget == b]
+        sampled.append(max(cand, key=lambda i: len(specs[i].steps)))
+    unit_rows, kept, max_n = _caps(cfg, specs)
+    run = SampledBatch(cfg, cfg.index, specs, sampled=sampled, layers_checked=[0, 35],
+                       budgets=[s.budget for s in specs], window=cfg.window, unit_rows=unit_rows,
+                       kept_rows=kept, max_step=max_n, tol=BF16_TOL, check_every=3,
+                       listen_call="fused", label="cfg2 full")
+    try:
+        run.run()
+    finally:
+        run.close()
+    print(f"[cfg2 full] evicting stream-steps {run.evictions}, unmet {run.unmet_steps}, "
+          f"attention checks {run.attn_checks}, max err {run.max_err:.3e}", flush=True)
+    assert run.evictions > 1000 and run.unmet_steps > 0 and run.attn_checks > 200
+
+
+@pytest.mark.parametrize("decode_call", ["decode", "fused"])
+def test_config3_full_decode_batched(gpu, decode_call):
+    cfg = CONFIGS[3]
+    specs = make_workload(cfg).streams
+    unit_rows, kept, max_n = _caps(cfg, specs, extra=cfg.decode_steps)
+    run = SampledBatch(cfg, cfg.index, specs, sampled=[0, 63], layers_checked=[0, 35],
+                       budgets=[cfg.budget] * len(specs), window=cfg.window, unit_rows=unit_rows,
+                       kept_rows=kept, max_step=max_n, tol=BF16_TOL, check_every=1,
+                       listen_call="fill", decode_call=decode_call, label=f"cfg3 full {decode_call}")
+    try:
+        run.run()
+    finally:
+        run.close()
+    print(f"[cfg3 full {decode_call}] evicting stream-steps {run.evictions}, attention checks "
+          f"{run.attn_checks}, max err {run.max_err:.3e}", flush=True)
+    # attention is checked on the decode steps (the fill appends without attention)
+    assert run.attn_checks == 2 * 2 * cfg.decode_steps
+    assert run.evictions > 64 * 400
