@@ -17,6 +17,10 @@ one call per layer (rate = stream unit-steps/s).
 single-row response decode steps, all streams batched (rate = stream
 decode-steps/s).
 
+--workload copy: a plain device-to-device copy of 1 GiB (torch's copy
+kernel), the reference point for scaling the HBM byte counters of a profile
+and for the bandwidth a streaming kernel can reach on this device.
+
 Inputs are synthetic and seeded (synth/): stream structure exactly as the
 workload defines it; Q/K/V values come from a pool of pre-generated tensors
 already resident in HBM (values do not change the work done).
@@ -55,11 +59,13 @@ METRICS = {
                "unit-steps/s"),
     "decode": ("stream decode-steps/s (append+decode attn+evict), batch of 64 streams",
                "decode-steps/s"),
+    "copy": ("device copy bandwidth (read + write bytes per second)", "GB/s"),
 }
 DEFAULTS = {  # warmup, steps, profile steps
     "stream": (200, 400, 100),
     "varlen": (100, 400, 100),
     "decode": (20, 150, 30),
+    "copy": (3, 20, 0),
 }
 
 
@@ -493,7 +499,7 @@ def run_decode(args):
     alg = float(np.mean(R_log)) if R_log else 0.0
     mean_R = float(np.mean([r.stream_info(i).resident for i in range(S)]))
     r.close()
-    kname = "attn_mfma" if fused else "attn_valu"
+    kname = "attn_mfma" if "attn_mfma" in kern else "attn_valu"
     return {
         "value": S * timed_steps / (total_ms * 1e-3),
         "ms_per_step": total_ms / max(1, timed_steps),
@@ -512,6 +518,33 @@ def run_decode(args):
         "kernels_us": kern,
         "cpu_baseline": None,
     }
+
+
+# ------------------------------------------------------------------- copy reference
+def run_copy(args):
+    import torch
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n = 1 << 30
+    x = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    y = torch.empty_like(x)
+    for _ in range(args.warmup):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(args.steps):
+        y.copy_(x)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / args.steps
+    return {"value": 2 * n / (ms * 1e-3) / 1e9, "ms_per_step": ms,
+            "config": {"workload": "device copy of 1 GiB (read 1 GiB + write 1 GiB per step)",
+                       "bytes_read": n, "bytes_written": n},
+            "roofline": {"bound": "hbm", "kernel": "copy", "achieved": 2 * n / (ms * 1e-3) / 1e9,
+                         "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": 2 * n / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, "traffic": None},
+            "cpu_baseline": None}
 
 
 def main():
@@ -540,9 +573,10 @@ def main():
     args.steps = s if args.steps is None else args.steps
     args.profile_steps = p if args.profile_steps is None else args.profile_steps
     if args.seed is None:
-        args.seed = {"stream": 1, "varlen": 2, "decode": 3}[args.workload]
+        args.seed = {"stream": 1, "varlen": 2, "decode": 3, "copy": 0}[args.workload]
 
-    res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode}[args.workload](args)
+    res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode,
+           "copy": run_copy}[args.workload](args)
     metric, unit = METRICS[args.workload]
     result = {
         "metric": metric,
@@ -555,7 +589,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "u8" if args.workload == "copy" else "bf16",
         "data": "synthetic",
     }
     result.update(res)

@@ -423,40 +423,71 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
     Stage sa, sb;
     const int vkp = tid / CPR, vdc = tid - (tid / CPR) * CPR;  // V block: keys 2*vkp, 2*vkp+1
 
+    // Fast path: a tile of resident rows that lies inside one contiguous run of
+    // one region (kept rows, or ring slots that do not wrap) and holds none of
+    // the step's new rows is addressed as a per-tile base plus per-thread
+    // offsets that do not change between tiles.  Only addresses differ between
+    // the paths: each chunk is loaded by one instruction after the choice, so
+    // no path merges loaded registers (which would force a wait on the loads).
+    int koff[NK];
+#pragma unroll
+    for (int it = 0; it < NK; ++it) {
+        const int c = tid + kMfmaThreads * it;
+        koff[it] = (c / CPR) * D + (c - (c / CPR) * CPR) * 8;
+    }
+    const int voff = (2 * vkp) * D + vdc * 8;
+    // element offset of tile row 0 in its region, with *kept_region set; -1
+    // when the tile takes the general path
+    auto fast_base = [&](int kb, bool* kept_region) -> int {
+        if (kb + kTileKeys > newbase) return -1;
+        if (kb + kTileKeys <= kept) {
+            *kept_region = true;
+            return kb * D;
+        }
+        if (kb < kept) return -1;
+        int slot = head + (kb - kept);
+        if (slot >= ring_rows) slot -= ring_rows;
+        if (slot + kTileKeys > ring_rows) return -1;
+        *kept_region = false;
+        return slot * D;
+    };
+    // general path: source of logical row j's chunk `col` (rows past R read
+    // row R-1: such keys are masked and their V rows get weight 0)
+    auto k_src = [&](int j, int col) -> const uint16_t* {
+        j = j < R ? j : R - 1;
+        if (j >= newbase)
+            return k_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D + col * 8;
+        bool ik;
+        const int off = row_off(j, &ik);
+        return (ik ? kk : ku) + off + col * 8;
+    };
+    auto v_src = [&](int j, int col) -> const uint16_t* {
+        j = j < R ? j : R - 1;
+        if (j >= newbase)
+            return v_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D + col * 8;
+        bool ik;
+        const int off = row_off(j, &ik);
+        return (ik ? vk : vu) + off + col * 8;
+    };
+
     auto gload = [&](int t, Stage& sg) {
-        uint4* kreg = sg.k;
-        uint4* vreg = sg.v;
         const int kb = t * kTileKeys;
+        bool in_kept = false;
+        const int fb = fast_base(kb, &in_kept);
+        const uint16_t* kf = (in_kept ? kk : ku) + fb;
+        const uint16_t* vf = (in_kept ? vk : vu) + fb;
 #pragma unroll
         for (int it = 0; it < NK; ++it) {
             const int c = tid + kMfmaThreads * it;
             const int row = c / CPR, col = c - row * CPR;
-            const int j = kb + row;
-            if (j >= newbase && j < R) {
-                const uint16_t* src = k_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D;
-                kreg[it] = *reinterpret_cast<const uint4*>(src + col * 8);
-            } else if (j < R) {
-                bool ik;
-                const int off = row_off(j, &ik);
-                kreg[it] = *reinterpret_cast<const uint4*>((ik ? kk : ku) + off + col * 8);
-            } else {
-                kreg[it] = make_uint4(0, 0, 0, 0);
-            }
+            const uint16_t* src = fb >= 0 ? kf + koff[it] : k_src(kb + row, col);
+            sg.k[it] = *reinterpret_cast<const uint4*>(src);
         }
         if (tid < NVP) {
 #pragma unroll
             for (int r2 = 0; r2 < 2; ++r2) {
-                const int j = kb + 2 * vkp + r2;
-                if (j >= newbase && j < R) {
-                    vreg[r2] = *reinterpret_cast<const uint4*>(
-                        v_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D + vdc * 8);
-                } else if (j < R) {
-                    bool ik;
-                    const int off = row_off(j, &ik);
-                    vreg[r2] = *reinterpret_cast<const uint4*>((ik ? vk : vu) + off + vdc * 8);
-                } else {
-                    vreg[r2] = make_uint4(0, 0, 0, 0);
-                }
+                const uint16_t* src = fb >= 0 ? vf + voff + r2 * D : v_src(kb + 2 * vkp + r2, vdc);
+                sg.v[r2] = *reinterpret_cast<const uint4*>(src);
             }
         }
     };
@@ -464,15 +495,17 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
         const uint4* kreg = sg.k;
         const uint4* vreg = sg.v;
         const int kb = t * kTileKeys;
+        const bool has_new = kb + kTileKeys > newbase;  // uniform: tile holds new rows
 #pragma unroll
         for (int it = 0; it < NK; ++it) {
             const int c = tid + kMfmaThreads * it;
             const int row = c / CPR, col = c - row * CPR;
             const int j = kb + row;
             uint4 kv = kreg[it];
-            // the rotate-half partner chunk (dims +-D/2) of this row sits in lane ^ (CPR/2)
-            const uint4 pv = xor_lanes<CPR / 2>(kv);
-            if (j >= newbase && j < R) {
+            if (has_new && j >= newbase && j < R) {
+                // the rotate-half partner chunk (dims +-D/2) of this row sits in lane ^ (CPR/2);
+                // all lanes of a row take this branch together
+                const uint4 pv = xor_lanes<CPR / 2>(kv);
                 // fused append: rotate this new key chunk, then also store it to its ring slot
                 const int d0 = col * 8;
                 const bool lower = d0 < D / 2;
@@ -511,7 +544,7 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
 #pragma unroll
             for (int r2 = 0; r2 < 2; ++r2) {
                 const int j = kb + kk + r2;
-                if (j >= newbase && j < R) {  // fused append: V row chunk to its ring slot
+                if (has_new && j >= newbase && j < R) {  // fused append: V row chunk to its ring slot
                     bool ik;
                     const int off = row_off(j, &ik);
                     *reinterpret_cast<uint4*>(const_cast<uint16_t*>(vu) + off + vdc * 8) = vreg[r2];
@@ -622,15 +655,20 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
 #pragma unroll
                 for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, sacc[kb][e]);
             tmax = quad_max(tmax);
-            const float mn = fmaxf(mrun, tmax);
-            const float mu = (mn == -INFINITY) ? 0.f : mn;
-            if (__any(mn != mrun)) {
-                const float corr = __builtin_amdgcn_exp2f(mrun - mu);
+            // mrun is the reference the exponentials are taken against.  It is
+            // raised (and acc, lrun rescaled) only when a row's tile maximum
+            // exceeds it by more than 2^8 in the exp2 domain, so p stays <= 256
+            // and most tiles skip the rescale; acc and lrun share the reference,
+            // so acc / lrun is unchanged.
+            if (__any(tmax > mrun + 8.f)) {
+                const float mn = fmaxf(mrun, tmax);
+                const float corr = __builtin_amdgcn_exp2f(mrun - ((mn == -INFINITY) ? 0.f : mn));
                 lrun *= corr;
 #pragma unroll
                 for (int db = 0; db < DB; ++db) acc[db] *= corr;
+                mrun = mn;
             }
-            mrun = mn;
+            const float mu = (mrun == -INFINITY) ? 0.f : mrun;
             uint32_t pk[4][2];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) {
