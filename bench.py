@@ -195,12 +195,38 @@ class Runner:
         self.a2t.a2t_cache_destroy(self.cache)
 
 
-def roofline(kernel, kern, alg_bytes):
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_mfma_traffic.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_31224_amd", "csrc", "kernels.hip")
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of ``kernel`` in ``workload`` from the committed
+    rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE, scaled by a plain
+    copy's readings), or None when the summary was taken on other kernel
+    source than the one built here."""
+    import hashlib
+    import re
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+        sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    m = re.search(r"<!-- traffic-json (.*) -->", text)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_sha256") != sha:
+        return None
+    return rec.get(workload, {}).get(kernel, {}).get("bytes")
+
+
+def roofline(kernel, kern, alg_bytes, workload):
     us = kern.get(kernel, {}).get("avg_us")
     achieved = alg_bytes / (us * 1e-6) / 1e9 if us else None
     return {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBPS,
             "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS if achieved else None,
-            "traffic": None, "avg_launch_us": us, "alg_bytes_per_launch": alg_bytes}
+            "traffic": measured_traffic(workload, kernel), "avg_launch_us": us,
+            "alg_bytes_per_launch": alg_bytes}
 
 
 def timing_fields(step_ms, total_ms, steps, t_wall, t_enqueue):
@@ -311,7 +337,7 @@ def run_stream(args):
                      else "a2t_append_attn per layer",
             "seed": args.seed,
         },
-        "roofline": roofline("attn_mfma", kern, prof_attn_bytes),
+        "roofline": roofline("attn_mfma", kern, prof_attn_bytes, "stream"),
         "step_hbm": {"achieved_gbps": step_gbps, "frac": step_gbps / HBM_PEAK_GBPS,
                      "alg_bytes_per_step": tot_bytes / max(1, args.steps)},
         **timing_fields(step_ms, total_ms, args.steps, t_wall, t_enq),
@@ -408,7 +434,7 @@ def run_varlen(args):
             "calls": "a2t_append_attn per layer over all active streams, one a2t_evict per step",
             "seed": args.seed,
         },
-        "roofline": roofline("attn_mfma", kern, alg),
+        "roofline": roofline("attn_mfma", kern, alg, "varlen"),
         **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
         "kernels_us": kern,
         "streams_budget_unmet_at_end": unmet_streams,
@@ -513,7 +539,7 @@ def run_decode(args):
             "mean_resident_rows_at_end": mean_R,
             "seed": args.seed,
         },
-        "roofline": roofline(kname, kern, alg),
+        "roofline": roofline(kname, kern, alg, "decode"),
         **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
         "kernels_us": kern,
         "cpu_baseline": None,
