@@ -111,6 +111,31 @@ class OracleCache:
         self.peak = max(self.peak, self.resident)
         self.step_rows = n
 
+    def load_rows(self, seg: Sequence[int], pos: Sequence[int], unit: Sequence[int],
+                  k: Dict[int, np.ndarray], v: Dict[int, np.ndarray], step_rows: int) -> None:
+        """Set the resident state in one go: rows in cache order with their own
+        unit ids, keys rotated by their original positions (Sec. 3.3), exactly
+        what appending them step by step would store.  ``step_rows`` is the
+        row count of the newest step (the rows queries may come from)."""
+        seg = np.asarray(seg, np.uint8)
+        pos = np.asarray(pos, np.int64)
+        unit = np.asarray(unit, np.int64)
+        if self.resident:
+            raise OracleError("load_rows fills an empty cache")
+        if np.any(np.diff(pos) <= 0):
+            raise OracleError("positions must strictly increase")
+        if np.any(seg > SEG_RESPONSE) or np.any(np.diff(unit) < 0):
+            raise OracleError("unknown segment class or decreasing unit ids")
+        self.pos, self.seg, self.unit = pos.copy(), seg.copy(), unit.copy()
+        for l in self.layers:
+            self.k[l] = rope.rotate(np.asarray(k[l], np.float64), pos, self.theta)
+            self.v[l] = np.asarray(v[l], np.float64).copy()
+        if pos.shape[0]:
+            self.cur = int(unit.max())
+            self.last_pos = int(pos[-1])
+        self.peak = max(self.peak, self.resident)
+        self.step_rows = int(step_rows)
+
     # -- 2. attention ------------------------------------------------------------
     def attention(self, layer: int, q: np.ndarray, n_q: Optional[int] = None) -> np.ndarray:
         """Attention of the last ``n_q`` appended rows (queries ``q[n_q][Hq][D]``,

@@ -44,6 +44,8 @@ def replay_metadata(spec: StreamSpec, budget: int, window: int,
                     n_steps: Optional[int] = None, evict: bool = True) -> StreamTrace:
     """Run the eviction policy over the first ``n_steps`` steps of a stream."""
     n_steps = len(spec.steps) if n_steps is None else n_steps
+    if not evict:
+        return _replay_no_eviction(spec, n_steps)
     pos = np.zeros(0, np.int64)
     seg = np.zeros(0, np.uint8)
     unit = np.zeros(0, np.int64)
@@ -78,6 +80,28 @@ def replay_metadata(spec: StreamSpec, budget: int, window: int,
     return tr
 
 
+def _replay_no_eviction(spec: StreamSpec, n_steps: int) -> StreamTrace:
+    """Without eviction every appended row stays: the layout is the concatenation."""
+    tr = StreamTrace()
+    steps = spec.steps[:n_steps]
+    total = 0
+    for st in steps:
+        total += st.n
+        tr.steps.append(StepTrace(total, total, [], False, 0))
+    tr.peak = total
+    if steps:
+        tr.pos = np.concatenate([st.pos.astype(np.int64) for st in steps])
+        tr.seg = np.concatenate([st.seg for st in steps])
+        tr.unit = np.concatenate([np.full(st.n, st.unit, np.int64) for st in steps])
+        tr.src_step = np.concatenate([np.full(st.n, i, np.int64) for i, st in enumerate(steps)])
+        tr.src_row = np.concatenate([np.arange(st.n, dtype=np.int64) for st in steps])
+    else:
+        tr.pos = np.zeros(0, np.int64)
+        tr.seg = np.zeros(0, np.uint8)
+        tr.unit = tr.src_step = tr.src_row = np.zeros(0, np.int64)
+    return tr
+
+
 def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window: int,
            n_steps: int, layers: Sequence[int]) -> OracleCache:
     """Oracle cache holding the state of ``spec`` after its first ``n_steps`` steps.
@@ -89,7 +113,9 @@ def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window
     tr = replay_metadata(spec, budget, window, n_steps)
     cache = OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, layers,
                         theta=cfg.rope_theta, scale=cfg.scale)
-    # group consecutive survivors by (step) so each appended batch has one unit id
+    # regenerate each surviving row's values from its source step
+    k = {l: np.zeros((tr.pos.shape[0], cfg.n_kv_heads, cfg.head_dim)) for l in layers}
+    v = {l: np.zeros((tr.pos.shape[0], cfg.n_kv_heads, cfg.head_dim)) for l in layers}
     steps = tr.src_step
     starts = np.flatnonzero(np.r_[True, steps[1:] != steps[:-1]])
     ends = np.r_[starts[1:], steps.shape[0]]
@@ -97,9 +123,10 @@ def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window
         st = spec.steps[int(steps[a])]
         vals = step_values(cfg, seed, spec.stream, st.key, st.n, layers)
         rows = tr.src_row[a:b]
-        k = {l: vals["k"][i][rows] for i, l in enumerate(layers)}
-        v = {l: vals["v"][i][rows] for i, l in enumerate(layers)}
-        cache.append(tr.seg[a:b], tr.pos[a:b], int(tr.unit[a]), k, v)
+        for i, l in enumerate(layers):
+            k[l][a:b] = vals["k"][i][rows]
+            v[l][a:b] = vals["v"][i][rows]
+    cache.load_rows(tr.seg, tr.pos, tr.unit, k, v, step_rows=0)
     cache.peak = tr.peak
     # the newest unit and position may belong to rows that were just evicted
     if n_steps:

@@ -88,6 +88,43 @@ def test_replay_matches_cache_policy():
     np.testing.assert_array_equal(c.pos, tr.pos)
 
 
+def test_resume_without_eviction_at_a_decode_workload_shape():
+    # no-eviction replay (linear path) equals the policy replay under a budget it
+    # never exceeds; resume from it equals driving the cache step by step
+    cfg = CONFIGS[0]
+    spec = make_workload(cfg, seed=4, decode_steps=5).streams[0]
+    big = 10 ** 9
+    a = replay_metadata(spec, big, cfg.window, evict=False)
+    b = replay_metadata(spec, big, cfg.window, evict=True)
+    for x, y in zip(a.steps, b.steps):
+        assert (x.n_pre, x.n_post, x.units, x.budget_unmet) == (y.n_pre, y.n_post, y.units,
+                                                                y.budget_unmet)
+    assert a.peak == b.peak == spec.total_rows()
+    for name in ("pos", "seg", "unit", "src_step", "src_row"):
+        np.testing.assert_array_equal(getattr(a, name), getattr(b, name))
+    n = len(spec.steps)
+    full = OracleCache(4, 1, 64, [0], theta=cfg.rope_theta, scale=cfg.scale)
+    _drive(full, cfg, 4, spec, big, cfg.window, n)
+    res = resume(cfg, 4, spec, big, cfg.window, n, [0])
+    np.testing.assert_array_equal(res.k[0], full.k[0])
+    np.testing.assert_array_equal(res.v[0], full.v[0])
+    np.testing.assert_array_equal(res.unit, full.unit)
+
+
+def test_load_rows_validates():
+    c = OracleCache(1, 1, 4, [0])
+    z = {0: np.zeros((2, 1, 4))}
+    with pytest.raises(OracleError):
+        c.load_rows([1, 1], [3, 3], [0, 0], z, z, 2)      # positions not increasing
+    with pytest.raises(OracleError):
+        c.load_rows([1, 7], [3, 4], [0, 0], z, z, 2)      # unknown class
+    with pytest.raises(OracleError):
+        c.load_rows([1, 1], [3, 4], [1, 0], z, z, 2)      # unit ids decrease
+    c.load_rows([1, 3], [3, 4], [0, 0], z, z, 2)
+    with pytest.raises(OracleError):
+        c.load_rows([1, 3], [5, 6], [0, 0], z, z, 2)      # not empty
+
+
 def test_append_validation():
     c = OracleCache(1, 1, 4, [])
     c.append([1, 1], [3, 4], 0)
