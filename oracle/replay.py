@@ -9,7 +9,7 @@ long stream at unit k by regenerating only the surviving rows' values.
 from __future__ import annotations
 
 from dataclasses import dataclass, field
-from typing import List, Optional, Sequence
+from typing import Callable, Dict, List, Optional, Sequence
 
 import numpy as np
 
@@ -103,14 +103,18 @@ def _replay_no_eviction(spec: StreamSpec, n_steps: int) -> StreamTrace:
 
 
 def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window: int,
-           n_steps: int, layers: Sequence[int]) -> OracleCache:
+           n_steps: int, layers: Sequence[int], evict: bool = True,
+           values: Optional[Callable[[int], Dict[str, np.ndarray]]] = None) -> OracleCache:
     """Oracle cache holding the state of ``spec`` after its first ``n_steps`` steps.
 
     The surviving rows are re-appended in cache order with their original
     positions (so their keys get the rotation of those positions), with
-    values regenerated from the seeded generator for ``layers``.
+    values regenerated from the seeded generator for ``layers``.  With
+    ``evict`` false the stream is replayed without eviction (a control run).
+    ``values(step_index)`` may supply a step's generated values (arrays ``k``,
+    ``v`` of shape ``[len(layers)][n][Hkv][D]``) instead of regenerating them.
     """
-    tr = replay_metadata(spec, budget, window, n_steps)
+    tr = replay_metadata(spec, budget, window, n_steps, evict=evict)
     cache = OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, layers,
                         theta=cfg.rope_theta, scale=cfg.scale)
     # regenerate each surviving row's values from its source step
@@ -121,7 +125,8 @@ def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window
     ends = np.r_[starts[1:], steps.shape[0]]
     for a, b in zip(starts, ends):
         st = spec.steps[int(steps[a])]
-        vals = step_values(cfg, seed, spec.stream, st.key, st.n, layers)
+        vals = values(int(steps[a])) if values is not None else \
+            step_values(cfg, seed, spec.stream, st.key, st.n, layers)
         rows = tr.src_row[a:b]
         for i, l in enumerate(layers):
             k[l][a:b] = vals["k"][i][rows]

@@ -8,8 +8,15 @@ call per layer, then one a2t_evict.  What the oracle can afford is checked:
   oracle's metadata-only policy replay (eviction reads no K/V values);
 * every stream at the end: the device layout (pos, seg, unit per slot);
 * sampled streams on the checked layers: attention outputs at every
-  ``check_every``-th step and the stored K/V at the end, against an oracle
-  cache fed the same seeded values.
+  ``check_every``-th step (or at the global steps in ``check_steps``) and the
+  stored K/V at the end, against an oracle cache fed the same seeded values:
+  run in lockstep, or (``oracle="rebuild"``, for histories too long to carry
+  along) rebuilt from the policy replay and the seeded generator at each
+  checked step.
+
+``listen_call``: "fused" (a2t_append_attn per layer), "fill" (one all-layers
+a2t_append per listening step, no attention) or "fill_check" (fill, except
+fused calls on the checked steps).
 
 Only the sampled streams on the checked layers carry values from the seeded
 generator; every other (stream, layer) slice gets fixed seeded pool values.
@@ -29,8 +36,8 @@ from tests.harness import Mismatch, bf16_bits_to_f32, make_cache
 
 class SampledBatch:
     def __init__(self, cfg, seed, specs, *, sampled, layers_checked, budgets, window, unit_rows,
-                 kept_rows, max_step, tol, check_every=1, listen_call="fused",
-                 decode_call="decode", evict=True, label=""):
+                 kept_rows, max_step, tol, check_every=1, check_steps=None, listen_call="fused",
+                 decode_call="decode", evict=True, oracle="lockstep", label=""):
         import torch
         import paper_2609_31224_amd as a2t
         from oracle.cache import OracleCache
@@ -43,11 +50,14 @@ class SampledBatch:
         self.window, self.tol, self.check_every = window, tol, check_every
         self.listen_call, self.decode_call, self.evict = listen_call, decode_call, evict
         self.label = label
+        self.check_steps = None if check_steps is None else set(check_steps)
+        self.rebuild = oracle == "rebuild"
+        self.kept_vals = {}
         S, L = len(specs), cfg.n_layers
         self.cache = make_cache(cfg, S, unit_rows, kept_rows, max_step)
-        self.oracles = {i: OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim,
-                                       self.layers_checked, theta=cfg.rope_theta, scale=cfg.scale)
-                        for i in self.sampled}
+        self.oracles = {} if self.rebuild else {
+            i: OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, self.layers_checked,
+                           theta=cfg.rope_theta, scale=cfg.scale) for i in self.sampled}
         self.traces = [replay_metadata(s, b, window, evict=evict)
                        for s, b in zip(specs, self.budgets)]
         self.T = max(s.offset + len(s.steps) for s in specs)
@@ -102,16 +112,29 @@ class SampledBatch:
         decode = all(st.decode for _, st in act)
         vals = {i: step_values(cfg, self.seed, self.specs[i].stream, st.key, st.n,
                                self.layers_checked)
-                for i, st in act if i in self.oracles}
+                for i, st in act if i in self.sampled}
+        if self.rebuild:
+            # keep the sampled streams' K/V (the same values the GPU gets) for rebuilds
+            for i, vv in vals.items():
+                self.kept_vals.setdefault(i, []).append({"k": vv["k"], "v": vv["v"]})
+        check = (t in self.check_steps) if self.check_steps is not None else \
+            (t % self.check_every) == 0
+        if self.rebuild and check:
+            # the sampled streams' state before this step, rebuilt; then this step
+            from oracle.replay import resume
+            self.oracles = {i: resume(cfg, self.seed, self.specs[i], self.budgets[i], self.window,
+                                      t - self.specs[i].offset, self.layers_checked,
+                                      evict=self.evict, values=self.kept_vals[i].__getitem__)
+                            for i, _ in act if i in self.sampled}
         for i, st in act:
-            if i in vals:
+            if i in vals and i in self.oracles:
                 k = {l: vals[i]["k"][j] for j, l in enumerate(self.layers_checked)}
                 v = {l: vals[i]["v"][j] for j, l in enumerate(self.layers_checked)}
                 self.oracles[i].append(st.seg, st.pos, st.unit, k, v)
         pq, pk, pv = self.pq[:tot], self.pk[:tot], self.pv[:tot]
-        check = (t % self.check_every) == 0
         t0 = time.perf_counter()
-        if not decode and self.listen_call == "fill":
+        fill = self.listen_call == "fill" or (self.listen_call == "fill_check" and not check)
+        if not decode and fill:
             # all layers in one append call, no attention (the decode benchmark's fill)
             L = cfg.n_layers
             kall = pk.unsqueeze(0).expand(L, *pk.shape).contiguous()
@@ -151,12 +174,14 @@ class SampledBatch:
             if i in self.oracles and self.evict:
                 rec = self.oracles[i].evict(self.budgets[i], self.window)
                 assert rec.n_evicted == want
+        if self.rebuild:
+            self.oracles = {}
 
     def _check_attention(self, t, layer, act, offs, vals, o):
         og = None
         j = self.layers_checked.index(layer)
         for (i, st), off in zip(act, offs):
-            if i not in vals:
+            if i not in vals or i not in self.oracles:
                 continue
             if og is None:
                 og = o.to(self.torch.float32).cpu().numpy()
@@ -189,6 +214,12 @@ class SampledBatch:
             peak = a2t.a2t_stream_info_get(self.cache, i)["peak"]
             if peak != tr.peak:
                 raise Mismatch(f"{self.label} stream {i}: peak {peak} vs {tr.peak}")
+        if self.rebuild:
+            from oracle.replay import resume
+            self.oracles = {i: resume(self.cfg, self.seed, self.specs[i], self.budgets[i],
+                                      self.window, len(self.specs[i].steps), self.layers_checked,
+                                      evict=self.evict, values=self.kept_vals[i].__getitem__)
+                            for i in self.sampled}
         for i, o in self.oracles.items():
             for layer in self.layers_checked:
                 k, v = a2t.a2t_read_kv(self.cache, layer, i)

@@ -66,3 +66,40 @@ def test_config3_full_decode_batched(gpu, decode_call):
     # attention is checked on the decode steps (the fill appends without attention)
     assert run.attn_checks == 2 * 2 * cfg.decode_steps
     assert run.evictions > 64 * 400
+
+
+def test_config4_full_hour_long_with_control(gpu):
+    # 16 streams x 3600 units (budget 8192, window 60), then the same streams with no
+    # eviction (control, ~79 K resident rows each: ~188 GB of K/V in one cache).  Every
+    # stream's eviction counts, budget flags, final layout and peak are checked; attention
+    # of a sampled stream on the last layer at three steps, against a rebuilt oracle.
+    cfg = CONFIGS[4]
+    specs = make_workload(cfg).streams
+    T = max(len(s.steps) for s in specs)
+    peaks = {}
+    for evict in (True, False):
+        if evict:
+            unit_rows, kept, max_n = _caps(cfg, specs)
+        else:
+            unit_rows = max(s.total_rows() for s in specs) + 64
+            kept, max_n = 64, cfg.max_unit_rows
+        label = "cfg4 full " + ("evict" if evict else "control")
+        run = SampledBatch(cfg, cfg.index, specs, sampled=[5], layers_checked=[35],
+                           budgets=[cfg.budget] * len(specs), window=cfg.window,
+                           unit_rows=unit_rows, kept_rows=kept, max_step=max_n, tol=BF16_TOL,
+                           check_steps={T // 3 - 1, 2 * T // 3 - 1, T - 1},
+                           listen_call="fill_check", evict=evict, oracle="rebuild", label=label)
+        try:
+            run.run(progress_every=300)
+            peaks[evict] = max(tr.peak for tr in run.traces)
+        finally:
+            run.close()
+        print(f"[{label}] evicting stream-steps {run.evictions}, unmet {run.unmet_steps}, "
+              f"attention checks {run.attn_checks}, max err {run.max_err:.3e}, "
+              f"peak rows {peaks[evict]}", flush=True)
+        assert run.attn_checks == 3
+        if evict:
+            assert run.unmet_steps > 0 and run.evictions > 16 * 3000
+    reduction = 1.0 - peaks[True] / peaks[False]
+    print(f"[cfg4 full] peak reduction {reduction:.3f}", flush=True)
+    assert reduction > 0.8
