@@ -23,6 +23,8 @@
 #include <hip/hip_ext.h>
 #include <math.h>
 
+#include <cstdlib>
+
 #include <type_traits>
 
 namespace a2t {
@@ -742,6 +744,387 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT
     }
 }
 
+// ----------------------------------------------------------------- attn_tile
+// Same attention as attn_mfma_kernel with a deeper load pipeline: K and V
+// tiles go from HBM straight into a 4-stage LDS ring (global_load_lds, 16
+// bytes per lane, no staging registers), so three tiles are in flight while
+// one is computed.  Lane j of a DMA instruction fills LDS bytes [16j, 16j+16)
+// of its 1 KiB block; the lane's source address picks which logical 16-byte
+// chunk lands there, which implements the bank-conflict swizzles:
+//   K: physical chunk = logical ^ (row & (CPR-1))   (Q.K^T reads 16 rows of one chunk)
+//   V: physical chunk = logical ^ 2 (row & (CPR/2-1))  (transposed reads of 16 rows x 32 B)
+// V stays row-major; the P.V operand (8 keys of one dim per lane) is read with
+// two ds_read_b64_tr_b16: within each 16-lane group, result lane 4a+b element
+// r is element b of the 8 bytes addressed by source lane a+4r.  Waits are
+// explicit: before the barrier that publishes tile t each wave waits until
+// only its DMAs of later tiles are outstanding.
+constexpr int kTileStages = 4;
+
+template <int D>
+struct TileBuf {
+    uint16_t k[kTileKeys * D];
+    uint16_t v[kTileKeys * D];
+};
+
+typedef short short4_t __attribute__((ext_vector_type(4)));
+
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt left alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// workgroup barrier that the compiler may not move memory accesses across; no
+// memory fence (the waits that make DMA'd data visible are explicit)
+__device__ __forceinline__ void barrier_only() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void dma16(const void* src, uint16_t* lds) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+__device__ __forceinline__ uint2 lds_tr16(const uint16_t* p) {
+    const short4_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) short4_t*)(p));
+    return __builtin_bit_cast(uint2, r);
+}
+
+template <int D, class BT>
+__global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT b,
+                                                                 const uint16_t* q, uint16_t* o,
+                                                                 const uint16_t* k_in,
+                                                                 const uint16_t* v_in) {
+    constexpr int KS = D / 32;                  // k-steps of Q.K^T
+    constexpr int DB = D / 16;                  // 16-dim blocks of O
+    constexpr int CPR = D / 8;                  // 16-byte chunks per row
+    constexpr int RPB = 512 / D;                // rows per 1 KiB DMA block
+    constexpr int OPS = kTileKeys / RPB / 8;    // K (and V) DMA blocks per wave per tile
+    constexpr int OPT = 2 * OPS;                // DMA instructions per wave per tile
+    constexpr int QPW = 16;
+    constexpr int QPP = QPW * (kMfmaThreads / 64);
+    static_assert(OPS >= 1 && RPB * CPR == 64, "tile shape");
+    __shared__ TileBuf<D> ring[kTileStages];
+
+    const AttnDesc d = b.d[blockIdx.z];
+    const int g = blockIdx.y, sp = blockIdx.x;
+    if (sp >= d.splits) return;
+    const int G = st.Hq / st.Hkv, nq = d.n_q, M = G * nq, R = d.R;
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
+    const int n_tiles = (R + kTileKeys - 1) / kTileKeys;
+    const int t0 = sp * n_tiles / d.splits, t1 = (sp + 1) * n_tiles / d.splits;
+    const int vis0 = R - nq;
+    const int kept = d.kept, head = d.head, ring_rows = st.unit_rows;
+    const int newbase = R - d.n_new;  // fused append: rows newbase .. R-1 come from k_in / v_in
+
+    const uint16_t* kk = reinterpret_cast<const uint16_t*>(st.k_kept) +
+                         pool_index(st, b.layer, d.s, g, st.kept_rows, 0);
+    const uint16_t* vk = reinterpret_cast<const uint16_t*>(st.v_kept) +
+                         pool_index(st, b.layer, d.s, g, st.kept_rows, 0);
+    uint16_t* ku = reinterpret_cast<uint16_t*>(st.k_unit) +
+                   pool_index(st, b.layer, d.s, g, st.unit_rows, 0);
+    uint16_t* vu = reinterpret_cast<uint16_t*>(st.v_unit) +
+                   pool_index(st, b.layer, d.s, g, st.unit_rows, 0);
+    auto row_off = [&](int j, bool* in_kept) -> int {
+        if (j < kept) {
+            *in_kept = true;
+            return j * D;
+        }
+        int slot = head + (j - kept);
+        if (slot >= ring_rows) slot -= ring_rows;
+        *in_kept = false;
+        return slot * D;
+    };
+    // element offset of a tile's row 0 when the whole tile is one contiguous
+    // run of resident rows without new rows (else -1)
+    auto fast_base = [&](int kb, bool* kept_region) -> int {
+        if (kb + kTileKeys > newbase) return -1;
+        if (kb + kTileKeys <= kept) {
+            *kept_region = true;
+            return kb * D;
+        }
+        if (kb < kept) return -1;
+        int slot = head + (kb - kept);
+        if (slot >= ring_rows) slot -= ring_rows;
+        if (slot + kTileKeys > ring_rows) return -1;
+        *kept_region = false;
+        return slot * D;
+    };
+    // this lane's DMA slots: block w*OPS+i holds tile rows (w*OPS+i)*RPB .. +RPB-1;
+    // lane j fills physical chunk j % CPR of row j / CPR of its block
+    uint32_t kofs[OPS], vofs[OPS];  // byte offsets inside a contiguous tile (fast path)
+#pragma unroll
+    for (int i = 0; i < OPS; ++i) {
+        const int pr = (w * OPS + i) * RPB + lane / CPR, pc = lane % CPR;
+        kofs[i] = (uint32_t)(pr * D + (pc ^ (pr & (CPR - 1))) * 8) * 2u;
+        vofs[i] = (uint32_t)(pr * D + (pc ^ (2 * (pr & (CPR / 2 - 1)))) * 8) * 2u;
+    }
+    auto src_of = [&](const uint16_t* reg_kept, const uint16_t* reg_ring, const uint16_t* in,
+                      int j, int ch) -> const uint16_t* {
+        j = j < R ? j : R - 1;  // rows past R read row R-1: masked keys, zero weight
+        if (j >= newbase) return in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D + ch * 8;
+        bool ik;
+        const int off = row_off(j, &ik);
+        return (ik ? reg_kept : reg_ring) + off + ch * 8;
+    };
+    // DMAs write LDS only, so the two paths need not share registers: the fast
+    // path is a scalar tile base plus 32-bit lane offsets
+    auto issue = [&](int t, TileBuf<D>& buf) {
+        const int kb = t * kTileKeys;
+        bool in_kept = false;
+        const int fb = fast_base(kb, &in_kept);
+        if (fb >= 0) {
+            const char* kf = reinterpret_cast<const char*>((in_kept ? kk : ku) + fb);
+            const char* vf = reinterpret_cast<const char*>((in_kept ? vk : vu) + fb);
+#pragma unroll
+            for (int i = 0; i < OPS; ++i) {
+                dma16(kf + kofs[i], &buf.k[(w * OPS + i) * 512]);
+                dma16(vf + vofs[i], &buf.v[(w * OPS + i) * 512]);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < OPS; ++i) {
+                const int pr = (w * OPS + i) * RPB + lane / CPR, pc = lane % CPR;
+                dma16(src_of(kk, ku, k_in, kb + pr, pc ^ (pr & (CPR - 1))), &buf.k[(w * OPS + i) * 512]);
+                dma16(src_of(vk, vu, v_in, kb + pr, pc ^ (2 * (pr & (CPR / 2 - 1)))),
+                      &buf.v[(w * OPS + i) * 512]);
+            }
+        }
+    };
+    // fused append on a tile holding the step's rows: rotate their keys in LDS
+    // (rotate-half partner = logical chunk ^ CPR/2 of the same row) and store
+    // K and V rows to their ring slots.  Every wave calls it (barriers inside).
+    auto fixup = [&](int t, TileBuf<D>& buf) {
+        const int kb = t * kTileKeys;
+        constexpr int PER = kTileKeys * CPR / kMfmaThreads;
+#pragma unroll 1
+        for (int e = 0; e < PER; ++e) {
+            const int idx = tid + kMfmaThreads * e, r = idx / CPR, c = idx % CPR, j = kb + r;
+            const bool mine = j >= newbase && j < R;
+            uint4 rot = make_uint4(0, 0, 0, 0), vv = rot;
+            if (mine) {
+                const uint4 kv = *reinterpret_cast<const uint4*>(&buf.k[r * D + (c ^ (r & (CPR - 1))) * 8]);
+                const int cp = c ^ (CPR / 2);
+                const uint4 pv = *reinterpret_cast<const uint4*>(&buf.k[r * D + (cp ^ (r & (CPR - 1))) * 8]);
+                vv = *reinterpret_cast<const uint4*>(&buf.v[r * D + (c ^ (2 * (r & (CPR / 2 - 1)))) * 8]);
+                const int d0 = c * 8;
+                const bool lower = d0 < D / 2;
+                const int i0 = lower ? d0 : d0 - D / 2;
+                const float4* cs4 = reinterpret_cast<const float4*>(
+                    st.rope + ((int64_t)d.s * st.max_step_rows + (j - newbase)) * (D / 2) + i0);
+                const uint32_t xw[4] = {kv.x, kv.y, kv.z, kv.w};
+                const uint32_t yw[4] = {pv.x, pv.y, pv.z, pv.w};
+                uint32_t ow[4];
+#pragma unroll
+                for (int e2 = 0; e2 < 4; ++e2) {
+                    const float4 c4 = cs4[e2];
+                    const float x0 = __uint_as_float(xw[e2] << 16), x1 = __uint_as_float(xw[e2] & 0xffff0000u);
+                    const float y0 = __uint_as_float(yw[e2] << 16), y1 = __uint_as_float(yw[e2] & 0xffff0000u);
+                    const float r0 = lower ? x0 * c4.x - y0 * c4.y : x0 * c4.x + y0 * c4.y;
+                    const float r1 = lower ? x1 * c4.z - y1 * c4.w : x1 * c4.z + y1 * c4.w;
+                    ow[e2] = pack_bf16x2(r0, r1);
+                }
+                rot = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+            }
+            __syncthreads();  // every partner chunk of this pass was read before any is overwritten
+            if (mine) {
+                *reinterpret_cast<uint4*>(&buf.k[r * D + (c ^ (r & (CPR - 1))) * 8]) = rot;
+                bool ik;
+                const int off = row_off(j, &ik);
+                *reinterpret_cast<uint4*>(ku + off + c * 8) = rot;
+                *reinterpret_cast<uint4*>(vu + off + c * 8) = vv;
+            }
+            __syncthreads();  // rotated keys visible; the stores are done before later waits count
+        }
+    };
+
+    const float2* rope = st.rope + ((int64_t)d.s * st.max_step_rows + d.rope_row0) * (D / 2);
+
+    for (int qg0 = 0; qg0 < M; qg0 += QPP) {
+        const int mw = qg0 + QPW * w;
+        const bool active = mw < M;
+        const int mq = mw + l16;
+
+        // Q^T operand loads go out before the first tiles' DMA so both overlap
+        uint4 qraw[KS];
+        float4 cs[KS / 2][4];
+        if (mq < M) {
+            const int i = mq / G, hh = mq - i * G;
+            const uint16_t* qp = q + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
+            const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)i * (D / 2));
+#pragma unroll
+            for (int s = 0; s < KS; ++s) qraw[s] = *reinterpret_cast<const uint4*>(qp + 32 * s + 8 * lg);
+#pragma unroll
+            for (int s = 0; s < KS / 2; ++s)
+#pragma unroll
+                for (int e2 = 0; e2 < 4; ++e2) cs[s][e2] = cs4[(32 * s + 8 * lg) / 2 + e2];
+        }
+        if (t0 < t1) issue(t0, ring[0]);
+        if (t0 + 1 < t1) issue(t0 + 1, ring[1]);
+        if (t0 + 2 < t1) issue(t0 + 2, ring[2]);
+
+        // Q^T operand: rotated, scaled by scale*log2(e), bf16
+        bf16x8 qop[KS];
+        {
+            float x[KS][8];
+            if (mq < M) {
+#pragma unroll
+                for (int s = 0; s < KS; ++s) {
+                    const uint32_t rw[4] = {qraw[s].x, qraw[s].y, qraw[s].z, qraw[s].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        x[s][2 * e] = __uint_as_float(rw[e] << 16);
+                        x[s][2 * e + 1] = __uint_as_float(rw[e] & 0xffff0000u);
+                    }
+                }
+#pragma unroll
+                for (int s = 0; s < KS / 2; ++s) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float4 c4 = cs[s][e >> 1];
+                        const float cc = (e & 1) ? c4.z : c4.x, sn = (e & 1) ? c4.w : c4.y;
+                        const float a = x[s][e], bb = x[s + KS / 2][e];
+                        x[s][e] = (a * cc - bb * sn) * st.scale_log2e;
+                        x[s + KS / 2][e] = (bb * cc + a * sn) * st.scale_log2e;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int s = 0; s < KS; ++s)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
+            }
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                qop[s] = __builtin_bit_cast(
+                    bf16x8, make_uint4(pack_bf16x2(x[s][0], x[s][1]), pack_bf16x2(x[s][2], x[s][3]),
+                                       pack_bf16x2(x[s][4], x[s][5]), pack_bf16x2(x[s][6], x[s][7])));
+        }
+
+        float mrun = -INFINITY, lrun = 0.f;
+        f32x4 acc[DB];
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int lim = (mq < M) ? vis0 + mq / G : -1;
+
+        auto compute = [&](int t, const TileBuf<D>& buf) {
+            const int kbase = t * kTileKeys;
+            f32x4 sacc[4];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) sacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb) {
+                    const int r = kb * 16 + l16, c = 4 * s + lg;
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(&buf.k[r * D + (c ^ (r & (CPR - 1))) * 8]);
+                    sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[s], sacc[kb], 0, 0, 0);
+                }
+            }
+            if (kbase + kTileKeys - 1 > vis0) {
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (kbase + kb * 16 + 4 * lg + e > lim) sacc[kb][e] = -INFINITY;
+            }
+            float tmax = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, sacc[kb][e]);
+            tmax = quad_max(tmax);
+            // lazily raised softmax reference: rescale only on a jump above 2^8
+            if (__any(tmax > mrun + 8.f)) {
+                const float mn = fmaxf(mrun, tmax);
+                const float corr = __builtin_amdgcn_exp2f(mrun - ((mn == -INFINITY) ? 0.f : mn));
+                lrun *= corr;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) acc[db] *= corr;
+                mrun = mn;
+            }
+            const float mu = (mrun == -INFINITY) ? 0.f : mrun;
+            uint32_t pk[4][2];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                float p[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    p[e] = __builtin_amdgcn_exp2f(sacc[kb][e] - mu);
+                    lrun += p[e];
+                }
+                pk[kb][0] = pack_bf16x2(p[0], p[1]);
+                pk[kb][1] = pack_bf16x2(p[2], p[3]);
+            }
+            // k-slots 8*lg+0..3 hold keys 32c + 4lg + 0..3 and 8*lg+4..7 keys 32c+16+4lg+0..3
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const bf16x8 pop = __builtin_bit_cast(
+                    bf16x8, make_uint4(pk[2 * c][0], pk[2 * c][1], pk[2 * c + 1][0], pk[2 * c + 1][1]));
+                const int r0 = 32 * c + 4 * lg + (l16 >> 2);   // source row of this lane's tr read
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const int dim = db * 16 + 4 * (l16 & 3);
+                    const int ch = dim >> 3, half = dim & 7;
+                    const uint2 lo = lds_tr16(&buf.v[r0 * D + ((ch ^ (2 * (r0 & (CPR / 2 - 1)))) << 3) + half]);
+                    const int r1 = r0 + 16;
+                    const uint2 hi = lds_tr16(&buf.v[r1 * D + ((ch ^ (2 * (r1 & (CPR / 2 - 1)))) << 3) + half]);
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+                    acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pop, acc[db], 0, 0, 0);
+                }
+            }
+        };
+
+        // one tile: wait for its DMA (only later tiles' DMA may stay in flight),
+        // publish it, refill the stage freed by the previous tile, compute
+        auto step = [&](int t, TileBuf<D>& cur, TileBuf<D>& nxt) {
+            const int rem = t1 - 1 - t;
+            if (rem >= 2)
+                wait_vmem<2 * OPT>();
+            else if (rem == 1)
+                wait_vmem<OPT>();
+            else
+                wait_vmem<0>();
+            barrier_only();
+            if (t * kTileKeys + kTileKeys > newbase && newbase < R) fixup(t, cur);
+            if (t + kTileStages - 1 < t1) issue(t + kTileStages - 1, nxt);
+            if (active) compute(t, cur);
+        };
+#pragma unroll 1
+        for (int t = t0; t < t1; ++t) {
+            const int k = (t - t0) & (kTileStages - 1);
+            step(t, ring[k], ring[(k + kTileStages - 1) & (kTileStages - 1)]);
+        }
+
+        if (active) lrun = quad_sum(lrun);
+        if (active && mq < M) {
+            const int i = mq / G, hh = mq - i * G;
+            if (d.splits == 1) {
+                const float inv = 1.f / lrun;
+                uint16_t* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const f32x4 a = acc[db];
+                    *reinterpret_cast<uint2*>(op + db * 16 + 4 * lg) =
+                        make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
+                }
+            } else {
+                float* po = st.ws + d.ws_off;
+                float* prow = po + (((int64_t)sp * st.Hkv + g) * M + mq) * D;
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+                    *reinterpret_cast<f32x4*>(prow + db * 16 + 4 * lg) = acc[db];
+                if (lg == 0) {
+                    float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
+                    *reinterpret_cast<float2*>(pml + (((int64_t)sp * st.Hkv + g) * M + mq) * 2) =
+                        make_float2(mrun, lrun);
+                }
+            }
+        }
+        __syncthreads();  // the stages are reused by the next pass over the keys
+    }
+}
+
 // ----------------------------------------------------------------- attn_merge
 // grid (row blocks, kv head, stream); each thread owns 4 output elements of
 // one query row.  The splits are read 16 at a time (all loads of a batch in
@@ -956,16 +1339,30 @@ hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* 
     const dim3 grid(b.max_splits, st.Hkv, b.count);
     const uint16_t* qq = static_cast<const uint16_t*>(q);
     uint16_t* oo = static_cast<uint16_t*>(o);
+    // A2T_ATTN_V1=1 selects the register-staged kernel (comparison runs)
+    static const bool staged = [] {
+        const char* e = std::getenv("A2T_ATTN_V1");
+        return e && e[0] == '1';
+    }();
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
-        if (st.D == 128)
-            A2T_DISPATCH((attn_mfma_kernel<128, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
-                               qq, oo, ki, vi);
-        else if (st.D == 64)
-            A2T_DISPATCH((attn_mfma_kernel<64, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
-                               qq, oo, ki, vi);
-        else
+        if (st.D == 128) {
+            if (staged)
+                A2T_DISPATCH((attn_mfma_kernel<128, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
+                             qq, oo, ki, vi);
+            else
+                A2T_DISPATCH((attn_tile_kernel<128, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
+                             qq, oo, ki, vi);
+        } else if (st.D == 64) {
+            if (staged)
+                A2T_DISPATCH((attn_mfma_kernel<64, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
+                             qq, oo, ki, vi);
+            else
+                A2T_DISPATCH((attn_tile_kernel<64, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
+                             qq, oo, ki, vi);
+        } else {
             return hipErrorInvalidValue;
+        }
         return hipGetLastError();
     });
 }
