@@ -212,24 +212,58 @@ int check_streams(a2t_cache* c, int32_t n, const int32_t* ids) {
 
 bool is_evictable(uint8_t seg) { return seg == A2T_SEG_ACOUSTIC || seg == A2T_SEG_DELIM; }
 
-// Splits of the key range for one attention launch.
-int choose_splits(const a2t_cache* c, int n_desc, int max_R, int64_t floats_per_split_all) {
-    const int n_tiles = std::max(1, (max_R + kTileKeys - 1) / kTileKeys);
-    int sp;
-    if (c->force_splits > 0) {
-        sp = c->force_splits;
+// Key splits per stream for one attention launch.  A workgroup of the MFMA
+// kernel occupies a whole CU (its LDS ring), so a launch runs in rounds of
+// `slots` (= CU count) workgroups and takes about rounds x (tiles of its
+// largest workgroup + its fixed part).  For each tile budget per workgroup
+// (>= 2 tiles) every stream gets the fewest splits that respect it; the budget
+// with the lowest cost wins (ties: fewer workgroups, i.e. fewer split
+// partials).  The partials must fit the workspace.
+void plan_splits(const a2t_cache* c, int n, const int* tiles, const int64_t* floats_per_split,
+                 int* splits) {
+    if (c->force_splits <= 0) {
+        const int Hkv = c->cfg.n_kv_heads;
+        int max_tiles = 1;
+        for (int i = 0; i < n; ++i) max_tiles = std::max(max_tiles, tiles[i]);
+        int64_t best_cost = INT64_MAX, best_w = 0;
+        int best_budget = max_tiles;
+        for (int budget = 2; budget <= std::max(2, max_tiles); ++budget) {
+            int64_t w = 0, ws = 0;
+            int largest = 1;
+            for (int i = 0; i < n; ++i) {
+                const int sp = std::max(1, std::min((tiles[i] + budget - 1) / budget, kMaxSplits));
+                w += (int64_t)sp * Hkv;
+                if (sp > 1) ws += sp * floats_per_split[i];
+                largest = std::max(largest, (tiles[i] + sp - 1) / sp);
+            }
+            if (ws > c->dev.ws_floats) continue;
+            // a workgroup's fixed part (first-load latency, partial write) ~ 2 tiles
+            const int64_t rounds = (w + c->target_wgs - 1) / c->target_wgs;
+            const int64_t cost = rounds * (largest + 2);
+            if (cost < best_cost || (cost == best_cost && w < best_w)) {
+                best_cost = cost;
+                best_w = w;
+                best_budget = budget;
+            }
+        }
+        for (int i = 0; i < n; ++i)
+            splits[i] = std::max(1, std::min((tiles[i] + best_budget - 1) / best_budget, kMaxSplits));
+        if (best_cost != INT64_MAX) return;
+        // nothing fits the workspace: fall through and shrink
     } else {
-        const int per = n_desc * c->cfg.n_kv_heads;
-        sp = std::max(1, (c->target_wgs + per - 1) / per);
-        // keep at least two tiles per split unless forced
-        sp = std::min(sp, std::max(1, n_tiles / 2));
+        for (int i = 0; i < n; ++i) splits[i] = std::max(1, std::min({c->force_splits, tiles[i], kMaxSplits}));
     }
-    sp = std::min(std::min(sp, n_tiles), kMaxSplits);
-    if (sp > 1) {
-        const int64_t cap = c->dev.ws_floats / std::max<int64_t>(1, floats_per_split_all);
-        sp = (int)std::min<int64_t>(sp, std::max<int64_t>(1, cap));
+    // shrink uniformly until the partials fit the workspace
+    for (;;) {
+        int64_t ws = 0;
+        int mx = 1;
+        for (int i = 0; i < n; ++i) {
+            if (splits[i] > 1) ws += splits[i] * floats_per_split[i];
+            mx = std::max(mx, splits[i]);
+        }
+        if (ws <= c->dev.ws_floats || mx == 1) break;
+        for (int i = 0; i < n; ++i) splits[i] = std::max(1, splits[i] / 2);
     }
-    return std::max(1, sp);
 }
 
 // One attention launch (plus merge) over up to kMaxDesc streams.
@@ -242,15 +276,16 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     b.count = n;
     b.layer = layer;
     const int G = c->cfg.n_q_heads / c->cfg.n_kv_heads;
-    int max_R = 0, max_rows = 0;
-    int64_t floats_all = 0;
+    int max_rows = 0, tiles[kMaxDesc], nsplit[kMaxDesc];
+    int64_t floats[kMaxDesc];
     for (int i = 0; i < n; ++i) {
         const StreamState& s = c->ss[ids[i]];
-        max_R = std::max(max_R, s.resident());
+        tiles[i] = std::max(1, (s.resident() + kTileKeys - 1) / kTileKeys);
         max_rows = std::max(max_rows, n_q[i]);
-        floats_all += (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
+        floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
     }
-    const int splits = choose_splits(c, n, max_R, floats_all);
+    plan_splits(c, n, tiles, floats, nsplit);
+    int splits = 1;
     int64_t off = 0;
     for (int i = 0; i < n; ++i) {
         const StreamState& s = c->ss[ids[i]];
@@ -262,8 +297,8 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         d.n_q = n_q[i];
         d.q_row0 = q_row0[i];
         d.rope_row0 = s.step_rows - n_q[i];
-        const int n_tiles = (d.R + kTileKeys - 1) / kTileKeys;
-        d.splits = std::max(1, std::min(splits, n_tiles));
+        d.splits = nsplit[i];
+        splits = std::max(splits, nsplit[i]);
         d.n_new = in_row0 ? s.step_rows : 0;
         d.in_row0 = in_row0 ? in_row0[i] : 0;
         d.ws_off = off;
@@ -383,7 +418,14 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     c->tmp_nq.assign(k.n_streams, 0);
     c->tmp_row0.assign(k.n_streams, 0);
     c->tmp_in0.assign(k.n_streams, 0);
-    c->target_wgs = std::max(1, env_int("A2T_TARGET_WGS", 256));
+    {
+        // one workgroup of the attention kernel per CU: a launch runs in rounds of CU count
+        int cus = 0;
+        if (c->host_only ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, k.device) != hipSuccess || cus <= 0)
+            cus = 256;
+        c->target_wgs = std::max(1, env_int("A2T_TARGET_WGS", cus));
+    }
     c->force_splits = std::max(0, env_int("A2T_SPLITS", 0));
     c->force_valu = env_flag("A2T_FORCE_VALU");
 

@@ -784,10 +784,29 @@ __device__ __forceinline__ void barrier_only() {
 __device__ __forceinline__ void dma16(const void* src, uint16_t* lds) {
     __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
-__device__ __forceinline__ uint2 lds_tr16(const uint16_t* p) {
-    const short4_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (__attribute__((address_space(3))) short4_t*)(p));
-    return __builtin_bit_cast(uint2, r);
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)(p);
+}
+// Transposed LDS read issued as inline assembly: the compiler cannot tell which
+// LDS the builtin form reads and would wait for every outstanding DMA before
+// it.  The result is valid only after lds_wait_all() names it.
+template <int OFF>
+__device__ __forceinline__ uint2 lds_tr16_issue(uint32_t addr) {
+    uint2 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+// s_waitcnt lgkmcnt(0) that the listed values depend on
+__device__ __forceinline__ void lds_wait_all(uint2 (&a)[8], uint2 (&b)[8]) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(a[4]), "+v"(a[5]), "+v"(a[6]),
+                   "+v"(a[7]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]), "+v"(b[4]), "+v"(b[5]),
+                   "+v"(b[6]), "+v"(b[7]));
+}
+__device__ __forceinline__ void lds_wait_all(uint2 (&a)[4], uint2 (&b)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]),
+                   "+v"(b[3]));
 }
 
 template <int D, class BT>
@@ -891,6 +910,20 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
             }
         }
     };
+    // a tile index past the range issues the same number of DMAs, all lanes
+    // reading the first 16 bytes of the kept region into the (unused) stage, so
+    // every path has the same count of outstanding loads
+    auto issue_or_dummy = [&](int t, TileBuf<D>& buf) {
+        if (t < t1) {
+            issue(t, buf);
+        } else {
+#pragma unroll
+            for (int i = 0; i < OPS; ++i) {
+                dma16(kk, &buf.k[(w * OPS + i) * 512]);
+                dma16(kk, &buf.v[(w * OPS + i) * 512]);
+            }
+        }
+    };
     // fused append on a tile holding the step's rows: rotate their keys in LDS
     // (rotate-half partner = logical chunk ^ CPR/2 of the same row) and store
     // K and V rows to their ring slots.  Every wave calls it (barriers inside).
@@ -945,11 +978,18 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
         const bool active = mw < M;
         const int mq = mw + l16;
 
-        // Q^T operand loads go out before the first tiles' DMA so both overlap
+        // load order: tile t0, Q, tiles t0+1 and t0+2 (compiler barriers keep
+        // it), so the Q latency overlaps tile t0's and waiting for Q leaves the
+        // next two tiles in flight
+        if (t0 < t1) issue(t0, ring[0]);
+        asm volatile("" ::: "memory");
+        // unconditional loads (rows past M read row M-1 and are zeroed below): a
+        // branch here would merge loaded registers and force an early wait
         uint4 qraw[KS];
         float4 cs[KS / 2][4];
-        if (mq < M) {
-            const int i = mq / G, hh = mq - i * G;
+        {
+            const int mqc = mq < M ? mq : M - 1;
+            const int i = mqc / G, hh = mqc - i * G;
             const uint16_t* qp = q + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
             const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)i * (D / 2));
 #pragma unroll
@@ -959,40 +999,34 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 #pragma unroll
                 for (int e2 = 0; e2 < 4; ++e2) cs[s][e2] = cs4[(32 * s + 8 * lg) / 2 + e2];
         }
-        if (t0 < t1) issue(t0, ring[0]);
-        if (t0 + 1 < t1) issue(t0 + 1, ring[1]);
-        if (t0 + 2 < t1) issue(t0 + 2, ring[2]);
+        asm volatile("" ::: "memory");
+        issue_or_dummy(t0 + 1, ring[1]);
+        issue_or_dummy(t0 + 2, ring[2]);
 
         // Q^T operand: rotated, scaled by scale*log2(e), bf16
         bf16x8 qop[KS];
         {
             float x[KS][8];
-            if (mq < M) {
+            const float qs = mq < M ? st.scale_log2e : 0.f;
 #pragma unroll
-                for (int s = 0; s < KS; ++s) {
-                    const uint32_t rw[4] = {qraw[s].x, qraw[s].y, qraw[s].z, qraw[s].w};
+            for (int s = 0; s < KS; ++s) {
+                const uint32_t rw[4] = {qraw[s].x, qraw[s].y, qraw[s].z, qraw[s].w};
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        x[s][2 * e] = __uint_as_float(rw[e] << 16);
-                        x[s][2 * e + 1] = __uint_as_float(rw[e] & 0xffff0000u);
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    x[s][2 * e] = __uint_as_float(rw[e] << 16);
+                    x[s][2 * e + 1] = __uint_as_float(rw[e] & 0xffff0000u);
                 }
+            }
 #pragma unroll
-                for (int s = 0; s < KS / 2; ++s) {
+            for (int s = 0; s < KS / 2; ++s) {
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const float4 c4 = cs[s][e >> 1];
-                        const float cc = (e & 1) ? c4.z : c4.x, sn = (e & 1) ? c4.w : c4.y;
-                        const float a = x[s][e], bb = x[s + KS / 2][e];
-                        x[s][e] = (a * cc - bb * sn) * st.scale_log2e;
-                        x[s + KS / 2][e] = (bb * cc + a * sn) * st.scale_log2e;
-                    }
+                for (int e = 0; e < 8; ++e) {
+                    const float4 c4 = cs[s][e >> 1];
+                    const float cc = (e & 1) ? c4.z : c4.x, sn = (e & 1) ? c4.w : c4.y;
+                    const float a = x[s][e], bb = x[s + KS / 2][e];
+                    x[s][e] = (a * cc - bb * sn) * qs;
+                    x[s + KS / 2][e] = (bb * cc + a * sn) * qs;
                 }
-            } else {
-#pragma unroll
-                for (int s = 0; s < KS; ++s)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
             }
 #pragma unroll
             for (int s = 0; s < KS; ++s)
@@ -1001,6 +1035,15 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                                        pack_bf16x2(x[s][4], x[s][5]), pack_bf16x2(x[s][6], x[s][7])));
         }
 
+        uint32_t vtr_off[DB];
+        {
+            const int r0 = 4 * lg + (l16 >> 2);  // rows 32c + r0 and +16 share r0's swizzle
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int dim = db * 16 + 4 * (l16 & 3);
+                vtr_off[db] = (uint32_t)(r0 * D + (((dim >> 3) ^ (2 * (r0 & (CPR / 2 - 1)))) << 3) + (dim & 7)) * 2u;
+            }
+        }
         float mrun = -INFINITY, lrun = 0.f;
         f32x4 acc[DB];
 #pragma unroll
@@ -1056,23 +1099,29 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                 pk[kb][0] = pack_bf16x2(p[0], p[1]);
                 pk[kb][1] = pack_bf16x2(p[2], p[3]);
             }
-            // k-slots 8*lg+0..3 hold keys 32c + 4lg + 0..3 and 8*lg+4..7 keys 32c+16+4lg+0..3
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
+            // k-slots 8*lg+0..3 hold keys 32c + 4lg + 0..3 and 8*lg+4..7 keys
+            // 32c+16+4lg+0..3; this lane's transposed reads start at row 32c+4lg+(l16>>2)
+            // (+16) and dims 16db + 4(l16&3) (the row offsets are immediates)
+            const uint32_t vb = lds_addr(&buf.v[0]);
+            auto pv_step = [&](auto cc) {
+                constexpr int c = decltype(cc)::value;
                 const bf16x8 pop = __builtin_bit_cast(
                     bf16x8, make_uint4(pk[2 * c][0], pk[2 * c][1], pk[2 * c + 1][0], pk[2 * c + 1][1]));
-                const int r0 = 32 * c + 4 * lg + (l16 >> 2);   // source row of this lane's tr read
+                uint2 lo[DB], hi[DB];
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
-                    const int dim = db * 16 + 4 * (l16 & 3);
-                    const int ch = dim >> 3, half = dim & 7;
-                    const uint2 lo = lds_tr16(&buf.v[r0 * D + ((ch ^ (2 * (r0 & (CPR / 2 - 1)))) << 3) + half]);
-                    const int r1 = r0 + 16;
-                    const uint2 hi = lds_tr16(&buf.v[r1 * D + ((ch ^ (2 * (r1 & (CPR / 2 - 1)))) << 3) + half]);
-                    const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+                    lo[db] = lds_tr16_issue<c * 32 * D * 2>(vb + vtr_off[db]);
+                    hi[db] = lds_tr16_issue<(c * 32 + 16) * D * 2>(vb + vtr_off[db]);
+                }
+                lds_wait_all(lo, hi);
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(lo[db].x, lo[db].y, hi[db].x, hi[db].y));
                     acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pop, acc[db], 0, 0, 0);
                 }
-            }
+            };
+            pv_step(std::integral_constant<int, 0>{});
+            pv_step(std::integral_constant<int, 1>{});
         };
 
         // one tile: wait for its DMA (only later tiles' DMA may stay in flight),
@@ -1121,7 +1170,7 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                 }
             }
         }
-        __syncthreads();  // the stages are reused by the next pass over the keys
+        if (qg0 + QPP < M) __syncthreads();  // the stages are reused by the next pass over the keys
     }
 }
 
