@@ -128,7 +128,7 @@ class Runner:
     """Shared plumbing: the library, a cache on torch's current stream, and
     per-kernel dispatch timing."""
 
-    KERNELS = ("attn_mfma", "attn_valu", "attn_merge", "append", "step_meta", "evict")
+    KERNELS = ("attn_tile", "attn_valu", "attn_merge", "append", "step_meta", "evict")
 
     def __init__(self, cfg, n_streams, unit_rows, kept_rows, max_n):
         import torch
@@ -195,7 +195,7 @@ class Runner:
         self.a2t.a2t_cache_destroy(self.cache)
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_mfma_traffic.md")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_31224_amd", "csrc", "kernels.hip")
 
 
@@ -337,7 +337,7 @@ def run_stream(args):
                      else "a2t_append_attn per layer",
             "seed": args.seed,
         },
-        "roofline": roofline("attn_mfma", kern, prof_attn_bytes, "stream"),
+        "roofline": roofline("attn_tile", kern, prof_attn_bytes, "stream"),
         "step_hbm": {"achieved_gbps": step_gbps, "frac": step_gbps / HBM_PEAK_GBPS,
                      "alg_bytes_per_step": tot_bytes / max(1, args.steps)},
         **timing_fields(step_ms, total_ms, args.steps, t_wall, t_enq),
@@ -434,7 +434,7 @@ def run_varlen(args):
             "calls": "a2t_append_attn per layer over all active streams, one a2t_evict per step",
             "seed": args.seed,
         },
-        "roofline": roofline("attn_mfma", kern, alg, "varlen"),
+        "roofline": roofline("attn_tile", kern, alg, "varlen"),
         **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
         "kernels_us": kern,
         "streams_budget_unmet_at_end": unmet_streams,
@@ -525,7 +525,7 @@ def run_decode(args):
     alg = float(np.mean(R_log)) if R_log else 0.0
     mean_R = float(np.mean([r.stream_info(i).resident for i in range(S)]))
     r.close()
-    kname = "attn_mfma" if "attn_mfma" in kern else "attn_valu"
+    kname = "attn_tile" if "attn_tile" in kern else "attn_valu"
     return {
         "value": S * timed_steps / (total_ms * 1e-3),
         "ms_per_step": total_ms / max(1, timed_steps),

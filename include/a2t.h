@@ -246,8 +246,9 @@ int a2t_sync(a2t_cache* c);
 /* Kernel timing with HIP events on the cache's stream (for benchmarks).
  * kernel_filter: NULL disables timing; "" times every kernel; otherwise only
  * kernels whose name contains the string ("step_meta", "append",
- * "attn_mfma", "attn_valu", "attn_merge", "evict").  While enabled, each
- * matching launch is bracketed by two events.  a2t_kernel_time waits for the
+ * "attn_tile", "attn_valu", "attn_merge", "evict").  While enabled, each
+ * matching launch carries a start/stop event pair recorded at the dispatch's
+ * own begin and end.  a2t_kernel_time waits for the
  * stream, then reports for the kernels whose name contains `kernel` the
  * number of launches and their summed duration in milliseconds since the
  * last report, and resets those counters. */

@@ -312,9 +312,9 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     const bool valu = c->cfg.dtype == A2T_F32 || c->force_valu;
     hipError_t e;
     {
-        ProfScope ps(c, valu ? "attn_valu" : "attn_mfma");
+        ProfScope ps(c, valu ? "attn_valu" : "attn_tile");
         e = valu ? launch_attn_valu(c->dev, b, q, o, c->stream, ps.kt())
-                 : launch_attn_mfma(c->dev, b, q, o, k_in, v_in, c->stream, ps.kt());
+                 : launch_attn_tile(c->dev, b, q, o, k_in, v_in, c->stream, ps.kt());
     }
     if (e != hipSuccess) return hip_fail(c);
     if (splits > 1) {

@@ -147,7 +147,7 @@ hipError_t launch_append(const DevState& st, const AppendBatch& b, int n_layers,
                          const void* k, const void* v, hipStream_t stream, const KTimer& kt);
 // MFMA chunk attention (bf16 cache, D 64 or 128).  With k_in/v_in non-null it
 // also appends each stream's n_new newest rows (rotating K) from that input.
-hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* q, void* o,
+hipError_t launch_attn_tile(const DevState& st, const AttnBatch& b, const void* q, void* o,
                             const void* k_in, const void* v_in, hipStream_t stream,
                             const KTimer& kt);
 // VALU attention, one (row, kv head) per workgroup column (fp32 caches, decode).

@@ -6,10 +6,11 @@
 //   append      rotates the step's keys by their positions and stores K and V
 //               rows into the ring (Sec. 3.3: keys keep their original rotary
 //               positions; they are never re-encoded later).
-//   attn_mfma   causal chunk attention of a step's new rows over the resident
-//               cache, bf16 MFMA 16x16x32 for Q.K^T and P.V, online softmax
-//               with wave shuffles, key splits for parallelism; also bf16
-//               decode (one query row per stream).
+//   attn_tile   causal chunk attention of a step's new rows over the resident
+//               cache: 64-key tiles DMA'd into a 4-stage LDS ring, bf16 MFMA
+//               16x16x32 for Q.K^T and P.V, online softmax with wave
+//               shuffles, key splits for parallelism; also bf16 decode (one
+//               query row per stream).
 //   attn_valu   the same attention on the vector ALU, one query row per
 //               workgroup column: fp32 caches (chunk and decode).
 //   attn_merge  combines key-split partials (fixed order, deterministic).
@@ -22,8 +23,6 @@
 
 #include <hip/hip_ext.h>
 #include <math.h>
-
-#include <cstdlib>
 
 #include <type_traits>
 
@@ -311,19 +310,17 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(DevState st, BT b, const
     }
 }
 
-// ----------------------------------------------------------------- attn_mfma
+// ----------------------------------------------------------------- attn_tile
 // One workgroup = (key split, kv head g, stream), 8 waves.  The M = G*n_q
 // query rows of the head group are processed 128 at a time; each wave owns 16
-// of them.  Per 64-key tile, K (row-major) and V^T are staged in LDS by all
-// 512 threads, with the next tile's global loads issued before the current
-// tile's math.
+// of them.
 //
 // S^T = K . Q^T with mfma_f32_16x16x32_bf16: A = K rows (16 keys x 32 dims),
 // B = Q^T (32 dims x 16 queries); the accumulator gives lane l the scores of
 // keys 4*(l/16)+e, e<4, for query l%16.  P^T then feeds P.V directly as the
 // B operand of O^T = V^T . P^T: within a 32-key chunk, k-slot 8*(l/16)+j maps
 // to key 16*(j/4) + 4*(l/16) + j%4, which is exactly what lane l holds; the A
-// operand reads the same keys from V^T in LDS.  No cross-lane transposes.
+// operand reads the same keys of V.  No cross-lane transposes of P.
 constexpr int kMfmaThreads = 512;
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
@@ -347,408 +344,9 @@ __device__ __forceinline__ float quad_sum(float x) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// Value of lane ^ X (X = 8 or 4) within each 16-lane row, via DPP row rotation.
-template <int X>
-__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
-    static_assert(X == 8 || X == 4, "row rotation");
-    if constexpr (X == 8) {
-        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xf, 0xf, false);  // row_ror:8
-    } else {
-        // lane ^ 4 within 8-lane halves.  row_ror:N makes lane l read lane (l - N) mod 16, so
-        // lanes with (l & 7) < 4 (source l + 4) take row_ror:12 and the others row_ror:4.
-        const uint32_t up = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x12c, 0xf, 0xf, false);
-        const uint32_t dn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xf, 0xf, false);
-        return ((threadIdx.x & 7) < 4) ? up : dn;
-    }
-}
-template <int X>
-__device__ __forceinline__ uint4 xor_lanes(uint4 v) {
-    return make_uint4(xor_lane<X>(v.x), xor_lane<X>(v.y), xor_lane<X>(v.z), xor_lane<X>(v.w));
-}
-
-template <int D, class BT>
-__global__ __launch_bounds__(kMfmaThreads) void attn_mfma_kernel(DevState st, BT b,
-                                                                 const uint16_t* q, uint16_t* o,
-                                                                 const uint16_t* k_in,
-                                                                 const uint16_t* v_in) {
-    constexpr int KS = D / 32;      // k-steps of Q.K^T
-    constexpr int DB = D / 16;      // 16-row blocks of V^T
-    constexpr int CPR = D / 8;      // 16-byte chunks per K/V row
-    constexpr int KROW = D + 8;     // LDS row stride of K (bf16 elements)
-    constexpr int VROW = kTileKeys + 8;              // LDS row stride of V^T
-    constexpr int NK = kTileKeys * CPR / kMfmaThreads;  // K chunks per thread
-    constexpr int NVP = (kTileKeys / 2) * CPR;          // V (2-key x 8-dim) blocks per tile
-    constexpr int QPW = 16;                             // queries per wave
-    constexpr int QPP = QPW * (kMfmaThreads / 64);      // queries per pass
-    static_assert(NK >= 1 && NVP <= kMfmaThreads, "tile shape");
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kTileKeys * KROW];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VROW];
-
-    const AttnDesc d = b.d[blockIdx.z];
-    const int g = blockIdx.y, sp = blockIdx.x;
-    if (sp >= d.splits) return;
-    const int G = st.Hq / st.Hkv, nq = d.n_q, M = G * nq, R = d.R;
-    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
-    const int n_tiles = (R + kTileKeys - 1) / kTileKeys;
-    const int t0 = sp * n_tiles / d.splits, t1 = (sp + 1) * n_tiles / d.splits;
-    const int vis0 = R - nq;  // query row i sees keys 0 .. vis0 + i
-    const int kept = d.kept, head = d.head, ring_rows = st.unit_rows;
-    // fused append: keys newbase .. R-1 are this step's rows, read from the input
-    const int newbase = R - d.n_new;
-
-    const uint16_t* kk = reinterpret_cast<const uint16_t*>(st.k_kept) +
-                         pool_index(st, b.layer, d.s, g, st.kept_rows, 0);
-    const uint16_t* vk = reinterpret_cast<const uint16_t*>(st.v_kept) +
-                         pool_index(st, b.layer, d.s, g, st.kept_rows, 0);
-    const uint16_t* ku = reinterpret_cast<const uint16_t*>(st.k_unit) +
-                         pool_index(st, b.layer, d.s, g, st.unit_rows, 0);
-    const uint16_t* vu = reinterpret_cast<const uint16_t*>(st.v_unit) +
-                         pool_index(st, b.layer, d.s, g, st.unit_rows, 0);
-    // element offset of logical key j's row inside its region
-    auto row_off = [&](int j, bool* in_kept) -> int {
-        if (j < kept) {
-            *in_kept = true;
-            return j * D;
-        }
-        int slot = head + (j - kept);
-        if (slot >= ring_rows) slot -= ring_rows;
-        *in_kept = false;
-        return slot * D;
-    };
-
-    // two register stages: the loads of the next two tiles are in flight while
-    // the current tile is computed
-    struct Stage {
-        uint4 k[NK];
-        uint4 v[2];
-    };
-    Stage sa, sb;
-    const int vkp = tid / CPR, vdc = tid - (tid / CPR) * CPR;  // V block: keys 2*vkp, 2*vkp+1
-
-    // Fast path: a tile of resident rows that lies inside one contiguous run of
-    // one region (kept rows, or ring slots that do not wrap) and holds none of
-    // the step's new rows is addressed as a per-tile base plus per-thread
-    // offsets that do not change between tiles.  Only addresses differ between
-    // the paths: each chunk is loaded by one instruction after the choice, so
-    // no path merges loaded registers (which would force a wait on the loads).
-    int koff[NK];
-#pragma unroll
-    for (int it = 0; it < NK; ++it) {
-        const int c = tid + kMfmaThreads * it;
-        koff[it] = (c / CPR) * D + (c - (c / CPR) * CPR) * 8;
-    }
-    const int voff = (2 * vkp) * D + vdc * 8;
-    // element offset of tile row 0 in its region, with *kept_region set; -1
-    // when the tile takes the general path
-    auto fast_base = [&](int kb, bool* kept_region) -> int {
-        if (kb + kTileKeys > newbase) return -1;
-        if (kb + kTileKeys <= kept) {
-            *kept_region = true;
-            return kb * D;
-        }
-        if (kb < kept) return -1;
-        int slot = head + (kb - kept);
-        if (slot >= ring_rows) slot -= ring_rows;
-        if (slot + kTileKeys > ring_rows) return -1;
-        *kept_region = false;
-        return slot * D;
-    };
-    // general path: source of logical row j's chunk `col` (rows past R read
-    // row R-1: such keys are masked and their V rows get weight 0)
-    auto k_src = [&](int j, int col) -> const uint16_t* {
-        j = j < R ? j : R - 1;
-        if (j >= newbase)
-            return k_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D + col * 8;
-        bool ik;
-        const int off = row_off(j, &ik);
-        return (ik ? kk : ku) + off + col * 8;
-    };
-    auto v_src = [&](int j, int col) -> const uint16_t* {
-        j = j < R ? j : R - 1;
-        if (j >= newbase)
-            return v_in + ((int64_t)(d.in_row0 + (j - newbase)) * st.Hkv + g) * D + col * 8;
-        bool ik;
-        const int off = row_off(j, &ik);
-        return (ik ? vk : vu) + off + col * 8;
-    };
-
-    auto gload = [&](int t, Stage& sg) {
-        const int kb = t * kTileKeys;
-        bool in_kept = false;
-        const int fb = fast_base(kb, &in_kept);
-        const uint16_t* kf = (in_kept ? kk : ku) + fb;
-        const uint16_t* vf = (in_kept ? vk : vu) + fb;
-#pragma unroll
-        for (int it = 0; it < NK; ++it) {
-            const int c = tid + kMfmaThreads * it;
-            const int row = c / CPR, col = c - row * CPR;
-            const uint16_t* src = fb >= 0 ? kf + koff[it] : k_src(kb + row, col);
-            sg.k[it] = *reinterpret_cast<const uint4*>(src);
-        }
-        if (tid < NVP) {
-#pragma unroll
-            for (int r2 = 0; r2 < 2; ++r2) {
-                const uint16_t* src = fb >= 0 ? vf + voff + r2 * D : v_src(kb + 2 * vkp + r2, vdc);
-                sg.v[r2] = *reinterpret_cast<const uint4*>(src);
-            }
-        }
-    };
-    auto lstore = [&](int t, const Stage& sg) {
-        const uint4* kreg = sg.k;
-        const uint4* vreg = sg.v;
-        const int kb = t * kTileKeys;
-        const bool has_new = kb + kTileKeys > newbase;  // uniform: tile holds new rows
-#pragma unroll
-        for (int it = 0; it < NK; ++it) {
-            const int c = tid + kMfmaThreads * it;
-            const int row = c / CPR, col = c - row * CPR;
-            const int j = kb + row;
-            uint4 kv = kreg[it];
-            if (has_new && j >= newbase && j < R) {
-                // the rotate-half partner chunk (dims +-D/2) of this row sits in lane ^ (CPR/2);
-                // all lanes of a row take this branch together
-                const uint4 pv = xor_lanes<CPR / 2>(kv);
-                // fused append: rotate this new key chunk, then also store it to its ring slot
-                const int d0 = col * 8;
-                const bool lower = d0 < D / 2;
-                const int i0 = lower ? d0 : d0 - D / 2;
-                const float4* cs4 = reinterpret_cast<const float4*>(
-                    st.rope + ((int64_t)d.s * st.max_step_rows + (j - newbase)) * (D / 2) + i0);
-                const uint32_t xw[4] = {kv.x, kv.y, kv.z, kv.w};
-                const uint32_t yw[4] = {pv.x, pv.y, pv.z, pv.w};
-                uint32_t ow[4];
-#pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2) {
-                    const float4 c4 = cs4[e2];
-                    const float x0 = __uint_as_float(xw[e2] << 16), x1 = __uint_as_float(xw[e2] & 0xffff0000u);
-                    const float y0 = __uint_as_float(yw[e2] << 16), y1 = __uint_as_float(yw[e2] & 0xffff0000u);
-                    const float r0 = lower ? x0 * c4.x - y0 * c4.y : x0 * c4.x + y0 * c4.y;
-                    const float r1 = lower ? x1 * c4.z - y1 * c4.w : x1 * c4.z + y1 * c4.w;
-                    ow[e2] = pack_bf16x2(r0, r1);
-                }
-                kv = make_uint4(ow[0], ow[1], ow[2], ow[3]);
-                bool ik;
-                const int off = row_off(j, &ik);
-                *reinterpret_cast<uint4*>(const_cast<uint16_t*>(ku) + off + d0) = kv;
-            }
-            *reinterpret_cast<uint4*>(&Ks[row * KROW + col * 8]) = kv;
-        }
-        if (tid < NVP) {
-            // keys 2*vkp, 2*vkp+1 go to their k-slot positions: within a 32-key
-            // chunk, key 16h + 4q + e sits at 8q + 4h + e, so the 8 k-slots a
-            // lane feeds to one MFMA are contiguous in a V^T row
-            // The 16-byte chunks of a V^T row are XOR-swizzled by (row / 8) so that
-            // lanes writing different rows 8 apart land in different LDS banks.
-            const int kk = 2 * vkp, cch = kk >> 5, k = kk & 31;
-            const int vpos = 32 * cch + 8 * ((k & 15) >> 2) + 4 * (k >> 4) + (k & 3);
-            const uint32_t w0[4] = {vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w};
-            const uint32_t w1[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
-#pragma unroll
-            for (int r2 = 0; r2 < 2; ++r2) {
-                const int j = kb + kk + r2;
-                if (has_new && j >= newbase && j < R) {  // fused append: V row chunk to its ring slot
-                    bool ik;
-                    const int off = row_off(j, &ik);
-                    *reinterpret_cast<uint4*>(const_cast<uint16_t*>(vu) + off + vdc * 8) = vreg[r2];
-                }
-            }
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int wd = e >> 1;
-                const int row = vdc * 8 + e;
-                const int spos = ((((vpos >> 3) ^ (row >> 3)) & 7) << 3) | (vpos & 7);
-                const uint32_t pr = (e & 1) ? ((w0[wd] >> 16) | (w1[wd] & 0xffff0000u))
-                                            : ((w0[wd] & 0xffffu) | (w1[wd] << 16));
-                *reinterpret_cast<uint32_t*>(&Vt[row * VROW + spos]) = pr;
-            }
-        }
-    };
-
-    const float2* rope = st.rope + ((int64_t)d.s * st.max_step_rows + d.rope_row0) * (D / 2);
-
-    for (int qg0 = 0; qg0 < M; qg0 += QPP) {
-        const int mw = qg0 + QPW * w;
-        const bool active = mw < M;
-        // the first tiles' loads go out before the Q prologue so both latencies overlap
-        if (t0 < t1) gload(t0, sa);
-        if (t0 + 1 < t1) gload(t0 + 1, sb);
-
-        // Q^T operand: rotated, scaled by scale*log2(e), bf16.
-        bf16x8 qop[KS];
-        {
-            const int mq = mw + l16;
-            float x[KS][8];
-            if (mq < M) {
-                const int i = mq / G, hh = mq - i * G;
-                const uint16_t* qp = q + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
-                const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)i * (D / 2));
-                float4 cs[KS / 2][4];
-#pragma unroll
-                for (int s = 0; s < KS / 2; ++s)
-#pragma unroll
-                    for (int e2 = 0; e2 < 4; ++e2) cs[s][e2] = cs4[(32 * s + 8 * lg) / 2 + e2];
-#pragma unroll
-                for (int s = 0; s < KS; ++s) {
-                    const uint4 raw = *reinterpret_cast<const uint4*>(qp + 32 * s + 8 * lg);
-                    const uint32_t rw[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        x[s][2 * e] = __uint_as_float(rw[e] << 16);
-                        x[s][2 * e + 1] = __uint_as_float(rw[e] & 0xffff0000u);
-                    }
-                }
-#pragma unroll
-                for (int s = 0; s < KS / 2; ++s) {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const float4 c4 = cs[s][e >> 1];
-                        const float cc = (e & 1) ? c4.z : c4.x, sn = (e & 1) ? c4.w : c4.y;
-                        const float a = x[s][e], bb = x[s + KS / 2][e];
-                        x[s][e] = (a * cc - bb * sn) * st.scale_log2e;
-                        x[s + KS / 2][e] = (bb * cc + a * sn) * st.scale_log2e;
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int s = 0; s < KS; ++s)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
-            }
-#pragma unroll
-            for (int s = 0; s < KS; ++s)
-                qop[s] = __builtin_bit_cast(
-                    bf16x8, make_uint4(pack_bf16x2(x[s][0], x[s][1]), pack_bf16x2(x[s][2], x[s][3]),
-                                       pack_bf16x2(x[s][4], x[s][5]), pack_bf16x2(x[s][6], x[s][7])));
-        }
-
-        float mrun = -INFINITY, lrun = 0.f;
-        f32x4 acc[DB];
-#pragma unroll
-        for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const int mq = mw + l16;
-        const int lim = (mq < M) ? vis0 + mq / G : -1;
-
-        auto compute = [&](int t) {
-            const int kbase = t * kTileKeys;
-
-            f32x4 sacc[4];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) sacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                        &Ks[(kb * 16 + l16) * KROW + 32 * s + 8 * lg]);
-                    sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[s], sacc[kb], 0, 0, 0);
-                }
-            }
-            if (kbase + kTileKeys - 1 > vis0) {
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (kbase + kb * 16 + 4 * lg + e > lim) sacc[kb][e] = -INFINITY;
-            }
-
-            float tmax = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, sacc[kb][e]);
-            tmax = quad_max(tmax);
-            // mrun is the reference the exponentials are taken against.  It is
-            // raised (and acc, lrun rescaled) only when a row's tile maximum
-            // exceeds it by more than 2^8 in the exp2 domain, so p stays <= 256
-            // and most tiles skip the rescale; acc and lrun share the reference,
-            // so acc / lrun is unchanged.
-            if (__any(tmax > mrun + 8.f)) {
-                const float mn = fmaxf(mrun, tmax);
-                const float corr = __builtin_amdgcn_exp2f(mrun - ((mn == -INFINITY) ? 0.f : mn));
-                lrun *= corr;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) acc[db] *= corr;
-                mrun = mn;
-            }
-            const float mu = (mrun == -INFINITY) ? 0.f : mrun;
-            uint32_t pk[4][2];
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                float p[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    p[e] = __builtin_amdgcn_exp2f(sacc[kb][e] - mu);
-                    lrun += p[e];  // this lane's share of the row sum
-                }
-                pk[kb][0] = pack_bf16x2(p[0], p[1]);
-                pk[kb][1] = pack_bf16x2(p[2], p[3]);
-            }
-            bf16x8 pop[2];
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-                pop[c] = __builtin_bit_cast(
-                    bf16x8, make_uint4(pk[2 * c][0], pk[2 * c][1], pk[2 * c + 1][0], pk[2 * c + 1][1]));
-
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const int row = db * 16 + l16;
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                        &Vt[row * VROW + ((((4 * c + lg) ^ (row >> 3)) & 7) << 3)]);
-                    acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pop[c], acc[db], 0, 0, 0);
-                }
-            }
-        };
-        for (int t = t0; t < t1; t += 2) {
-            __syncthreads();  // every wave is done reading the previous tile
-            lstore(t, sa);
-            __syncthreads();
-            if (t + 2 < t1) gload(t + 2, sa);
-            if (active) compute(t);
-            if (t + 1 < t1) {
-                __syncthreads();
-                lstore(t + 1, sb);
-                __syncthreads();
-                if (t + 3 < t1) gload(t + 3, sb);
-                if (active) compute(t + 1);
-            }
-        }
-
-        if (active) lrun = quad_sum(lrun);
-        if (active && mq < M) {
-            const int i = mq / G, hh = mq - i * G;
-            if (d.splits == 1) {
-                const float inv = 1.f / lrun;
-                uint16_t* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const f32x4 a = acc[db];
-                    *reinterpret_cast<uint2*>(op + db * 16 + 4 * lg) =
-                        make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
-                }
-            } else {
-                float* po = st.ws + d.ws_off;
-                float* prow = po + (((int64_t)sp * st.Hkv + g) * M + mq) * D;
-#pragma unroll
-                for (int db = 0; db < DB; ++db)
-                    *reinterpret_cast<f32x4*>(prow + db * 16 + 4 * lg) = acc[db];
-                if (lg == 0) {
-                    float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
-                    *reinterpret_cast<float2*>(pml + (((int64_t)sp * st.Hkv + g) * M + mq) * 2) =
-                        make_float2(mrun, lrun);
-                }
-            }
-        }
-        __syncthreads();
-    }
-}
-
-// ----------------------------------------------------------------- attn_tile
-// Same attention as attn_mfma_kernel with a deeper load pipeline: K and V
-// tiles go from HBM straight into a 4-stage LDS ring (global_load_lds, 16
-// bytes per lane, no staging registers), so three tiles are in flight while
-// one is computed.  Lane j of a DMA instruction fills LDS bytes [16j, 16j+16)
+// Tiles of 64 keys go from HBM straight into a 4-stage LDS ring
+// (global_load_lds, 16 bytes per lane, no staging registers), so three tiles
+// are in flight while one is computed.  Lane j of a DMA instruction fills LDS bytes [16j, 16j+16)
 // of its 1 KiB block; the lane's source address picks which logical 16-byte
 // chunk lands there, which implements the bank-conflict swizzles:
 //   K: physical chunk = logical ^ (row & (CPR-1))   (Q.K^T reads 16 rows of one chunk)
@@ -1380,7 +978,7 @@ hipError_t launch_append(const DevState& st, const AppendBatch& b, int n_layers,
     });
 }
 
-hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* q, void* o,
+hipError_t launch_attn_tile(const DevState& st, const AttnBatch& b, const void* q, void* o,
                             const void* k_in, const void* v_in, hipStream_t stream,
                             const KTimer& kt) {
     const uint16_t* ki = static_cast<const uint16_t*>(k_in);
@@ -1388,27 +986,14 @@ hipError_t launch_attn_mfma(const DevState& st, const AttnBatch& b, const void* 
     const dim3 grid(b.max_splits, st.Hkv, b.count);
     const uint16_t* qq = static_cast<const uint16_t*>(q);
     uint16_t* oo = static_cast<uint16_t*>(o);
-    // A2T_ATTN_V1=1 selects the register-staged kernel (comparison runs)
-    static const bool staged = [] {
-        const char* e = std::getenv("A2T_ATTN_V1");
-        return e && e[0] == '1';
-    }();
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
         if (st.D == 128) {
-            if (staged)
-                A2T_DISPATCH((attn_mfma_kernel<128, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
-                             qq, oo, ki, vi);
-            else
-                A2T_DISPATCH((attn_tile_kernel<128, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
-                             qq, oo, ki, vi);
+            A2T_DISPATCH((attn_tile_kernel<128, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
+                         qq, oo, ki, vi);
         } else if (st.D == 64) {
-            if (staged)
-                A2T_DISPATCH((attn_mfma_kernel<64, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
-                             qq, oo, ki, vi);
-            else
-                A2T_DISPATCH((attn_tile_kernel<64, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
-                             qq, oo, ki, vi);
+            A2T_DISPATCH((attn_tile_kernel<64, B>), grid, dim3(kMfmaThreads), stream, kt, st, bb,
+                         qq, oo, ki, vi);
         } else {
             return hipErrorInvalidValue;
         }
