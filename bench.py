@@ -17,6 +17,12 @@ one call per layer (rate = stream unit-steps/s).
 single-row response decode steps, all streams batched (rate = stream
 decode-steps/s).
 
+--workload cadence: the ten-minute single stream in the side channel's call
+pattern: per unit one prefill chunk of the 17 acoustic/structural rows, then
+one decode step per side-channel token (opening delimiter, transcript tokens,
+closing delimiter), each step a2t_append_attn on every layer, and the budget
+check once per unit (rate = stream unit-steps/s).
+
 --workload copy: a plain device-to-device copy of 1 GiB (torch's copy
 kernel), the reference point for scaling the HBM byte counters of a profile
 and for the bandwidth a streaming kernel can reach on this device.
@@ -59,12 +65,15 @@ METRICS = {
                "unit-steps/s"),
     "decode": ("stream decode-steps/s (append+decode attn+evict), batch of 64 streams",
                "decode-steps/s"),
+    "cadence": ("stream unit-steps/s, side-channel cadence (prefill chunk + one decode step "
+                "per transcript token, all layers, eviction per unit)", "unit-steps/s"),
     "copy": ("device copy bandwidth (read + write bytes per second)", "GB/s"),
 }
 DEFAULTS = {  # warmup, steps, profile steps
     "stream": (200, 400, 100),
     "varlen": (100, 400, 100),
     "decode": (20, 150, 30),
+    "cadence": (200, 100, 30),
     "copy": (3, 20, 0),
 }
 
@@ -546,6 +555,84 @@ def run_decode(args):
     }
 
 
+# ------------------------------------------------------------------- side-channel cadence
+def run_cadence(args):
+    from synth.streams import make_cadence_workload
+    base = CONFIGS[1]
+    total_units = args.warmup + args.steps + args.profile_steps
+    cfg = dataclasses.replace(base, units=max(base.units, total_units))
+    spec = make_cadence_workload(cfg, seed=args.seed, units=total_units).streams[0]
+    L, Hq, Hkv, D = cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    max_n = cfg.max_unit_rows
+    keep_rows = sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in spec.steps)
+    unit_rows = max(cfg.budget, cfg.window * max_n) + 2 * max_n
+    r = Runner(cfg, 1, unit_rows, keep_rows + 64, max_n)
+    torch, lib, h = r.torch, r.lib, r.h
+    qp = r.pool((POOL, L, max_n, Hq, D), args.seed)
+    kp = r.pool((POOL, L, max_n, Hkv, D), args.seed + 1)
+    vp = r.pool((POOL, L, max_n, Hkv, D), args.seed + 2)
+    out = torch.empty(max_n, Hq, D, dtype=torch.bfloat16, device=r.dev)
+    ids = (C.c_int32 * 1)(0)
+    budget = (C.c_int32 * 1)(cfg.budget)
+    n_ev, unmet = (C.c_int32 * 1)(), (C.c_uint8 * 1)()
+    # the steps of each unit, marshalled
+    units = []
+    cur = []
+    for st in spec.steps:
+        cur.append(((C.c_int32 * 1)(st.n), (C.c_uint8 * st.n)(*st.seg.tolist()),
+                    (C.c_int32 * st.n)(*st.pos.tolist()), (C.c_int32 * 1)(st.unit)))
+        if st.evict:
+            units.append(cur)
+            cur = []
+    sq, skv = max_n * Hq * D * 2, max_n * Hkv * D * 2
+    R_log = []
+
+    def run_unit(u, record=False):
+        p = u % POOL
+        row = 0
+        for (nrows, seg, pos, unit) in units[u]:
+            for layer in range(L):
+                oq = ((p * L + layer) * max_n + row) * Hq * D * 2
+                okv = ((p * L + layer) * max_n + row) * Hkv * D * 2
+                meta = (seg, pos, unit) if layer == 0 else (None, None, None)
+                r.check(lib.a2t_append_attn(h, layer, 1, ids, nrows, kp.data_ptr() + okv,
+                                            vp.data_ptr() + okv, *meta, nrows, qp.data_ptr() + oq,
+                                            out.data_ptr()), "a2t_append_attn")
+            if record:
+                R_log.append((r.stream_info(0).resident, nrows[0]))
+            row += nrows[0]
+        r.check(lib.a2t_evict(h, 1, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
+
+    for u in range(args.warmup):
+        run_unit(u)
+    step_ms, total_ms, t_wall, t_enq = r.timed(lambda j: run_unit(args.warmup + j), args.steps)
+    p0 = args.warmup + args.steps
+    kern = r.profiled(lambda j: run_unit(p0 + j, record=True), args.profile_steps)
+    launches = len(R_log)
+    alg = float(np.mean([attn_bytes(R, n, cfg) for R, n in R_log])) if R_log else 0.0
+    steps_per_unit = sum(len(units[u]) for u in range(args.warmup, p0)) / max(1, args.steps)
+    r.close()
+    return {
+        "value": 1000.0 * args.steps / total_ms,
+        "ms_per_step": total_ms / args.steps,
+        "config": {
+            "workload": "ten-minute single stream, side-channel cadence: per unit a prefill chunk of "
+                        "17 acoustic/structural rows, then one decode step per side-channel token "
+                        "(2 delimiters + Poisson(3) transcript tokens); 36 layers, 32 query / 8 KV "
+                        "heads, head dim 128, bf16, budget 4096 rows, recent window 30 units",
+            "timed_units": [args.warmup, p0],
+            "calls_per_unit": steps_per_unit,
+            "calls": "a2t_append_attn per layer and step, one a2t_evict per unit",
+            "seed": args.seed,
+        },
+        "roofline": roofline("attn_tile", kern, alg, "cadence"),
+        **timing_fields(step_ms, total_ms, args.steps, t_wall, t_enq),
+        "kernels_us": kern,
+        "profiled_attention_calls": launches,
+        "cpu_baseline": None,
+    }
+
+
 # ------------------------------------------------------------------- copy reference
 def run_copy(args):
     import torch
@@ -599,10 +686,10 @@ def main():
     args.steps = s if args.steps is None else args.steps
     args.profile_steps = p if args.profile_steps is None else args.profile_steps
     if args.seed is None:
-        args.seed = {"stream": 1, "varlen": 2, "decode": 3, "copy": 0}[args.workload]
+        args.seed = {"stream": 1, "varlen": 2, "decode": 3, "cadence": 1, "copy": 0}[args.workload]
 
     res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode,
-           "copy": run_copy}[args.workload](args)
+           "cadence": run_cadence, "copy": run_copy}[args.workload](args)
     metric, unit = METRICS[args.workload]
     result = {
         "metric": metric,

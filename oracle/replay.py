@@ -63,7 +63,9 @@ def replay_metadata(spec: StreamSpec, budget: int, window: int,
         src_row = np.concatenate([src_row, np.arange(n, dtype=np.int64)])
         cur = max(cur, st.unit)
         tr.peak = max(tr.peak, pos.shape[0])
-        if not evict:
+        if not evict or not st.evict:
+            # Sec. 3.3 checks the budget after each duplex unit: a step that does
+            # not end its unit (a side-channel chunk or token) is not checked
             tr.steps.append(StepTrace(pos.shape[0], pos.shape[0], [], False, 0))
             continue
         plan = plan_eviction(seg, unit, budget, window, cur)

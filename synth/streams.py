@@ -105,12 +105,16 @@ CONFIGS: Dict[int, WorkloadConfig] = {
 
 @dataclass
 class UnitSpec:
-    """One step of one stream: a listening unit or a single decode row."""
+    """One step of one stream: a listening unit (or its prefill chunk) or a
+    single decode row.  ``evict``: the eviction check runs after this step
+    (after every step of a listening workload; in the side-channel cadence
+    once per duplex unit, after its closing delimiter)."""
     unit: int                 # unit id carried by every row of the step
     key: int                  # value-generator step key
     seg: np.ndarray           # uint8 [n]
     pos: np.ndarray           # int32 [n]
     decode: bool = False
+    evict: bool = True
 
     @property
     def n(self) -> int:
@@ -206,6 +210,36 @@ def make_workload(cfg: WorkloadConfig | int, seed: Optional[int] = None,
         streams.append(StreamSpec(stream=s, budget=int(budgets[s]), offset=int(offsets[s]),
                                   steps=steps))
     return Workload(config=cfg, seed=seed, streams=streams)
+
+
+CADENCE_KEY_STRIDE = 80   # value keys of unit u's steps: u * 80 + 0 .. 66
+
+
+def make_cadence_workload(cfg: WorkloadConfig | int, seed: Optional[int] = None,
+                          units: Optional[int] = None,
+                          n_streams: Optional[int] = None) -> Workload:
+    """The same sessions as ``make_workload`` (same draws, same rows and
+    positions), delivered in the side channel's call pattern (Sec. 3.1): per
+    duplex unit one prefill chunk of its acoustic/structural rows, then one
+    decode step per side-channel token -- the opening delimiter, the t
+    transcript tokens and the closing delimiter (a forced close at the 64-token
+    cap is the same row).  Every row keeps its unit id; the eviction check runs
+    once per unit, after the closing delimiter."""
+    base = make_workload(cfg, seed=seed, units=units, n_streams=n_streams, decode_steps=0)
+    streams = []
+    for s in base.streams:
+        steps = []
+        for st in s.steps:
+            a = int(np.sum(st.seg == SEG_ACOUSTIC))
+            k0 = st.unit * CADENCE_KEY_STRIDE
+            steps.append(UnitSpec(unit=st.unit, key=k0, seg=st.seg[:a].copy(),
+                                  pos=st.pos[:a].copy(), evict=False))
+            for r in range(a, st.n):
+                steps.append(UnitSpec(unit=st.unit, key=k0 + 1 + (r - a), seg=st.seg[r:r + 1].copy(),
+                                      pos=st.pos[r:r + 1].copy(), decode=True,
+                                      evict=(r == st.n - 1)))
+        streams.append(StreamSpec(stream=s.stream, budget=s.budget, offset=s.offset, steps=steps))
+    return Workload(config=base.config, seed=base.seed, streams=streams)
 
 
 def tiny_stream(units: Sequence[Sequence[int]], prefix: int = 0, start_pos: int = 0,

@@ -158,6 +158,10 @@ class SampledBatch:
                 if check and layer in self.layers_checked:
                     self._check_attention(t, layer, act, offs, vals, o)
         self.layer_loop_s += time.perf_counter() - t0
+        act = [(i, st) for i, st in act if st.evict]  # checked after the steps ending a unit
+        ids = [i for i, _ in act]
+        if not act:
+            return
         if self.evict:
             budgets = [self.budgets[i] for i in ids]
             n_ev, unmet = a2t.a2t_evict(self.cache, ids, budgets, self.window)

@@ -186,9 +186,15 @@ class Lockstep:
                 for l in self.layers_checked[:1]:
                     pre_kv[(i, l)] = a2t.a2t_read_kv(self.cache, l, i)
                     self._check_kv(i, l, *pre_kv[(i, l)], t)
-        budgets = [self.budgets[i] for i in ids]
-        n_ev, unmet = a2t.a2t_evict(self.cache, ids, budgets, self.window)
-        for j, (i, st) in enumerate(act):
+        # the eviction check runs after the steps that end a duplex unit
+        ev_act = [(i, st) for i, st in act if st.evict]
+        if not ev_act:
+            self.steps_done += 1
+            return
+        ev_ids = [i for i, _ in ev_act]
+        budgets = [self.budgets[i] for i in ev_ids]
+        n_ev, unmet = a2t.a2t_evict(self.cache, ev_ids, budgets, self.window)
+        for j, (i, st) in enumerate(ev_act):
             rec = self.oracles[i].evict(self.budgets[i], self.window)
             if int(n_ev[j]) != rec.n_evicted or bool(unmet[j]) != rec.plan.budget_unmet:
                 raise Mismatch(f"step {t} stream {i}: evicted {n_ev[j]}/{rec.n_evicted} "

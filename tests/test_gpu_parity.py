@@ -292,3 +292,52 @@ def test_errors_on_gpu_leave_cache_usable(gpu):
         assert a2t.a2t_stream_info_get(c, 0)["resident"] == 0
     finally:
         a2t.a2t_cache_destroy(c)
+
+
+# ---- side-channel cadence (Sec. 3.1): per unit a prefill chunk, then one decode step per
+# side-channel token; the budget is checked once per unit
+def test_cadence_config0_fp32(gpu):
+    from synth.streams import make_cadence_workload
+    cfg = CONFIGS[0]
+    spec = make_cadence_workload(cfg, seed=3).streams[0]
+    ls = Lockstep(cfg, 3, [spec], layers_checked=[0], n_layers=1, budgets=[cfg.budget],
+                  window=cfg.window, tol=F32_TOL, **_bounds([spec], cfg.budget))
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    _report(ls, "cadence cfg0 fp32")
+    assert ls.evictions > 10
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_cadence_config1_shape_bf16(gpu, fused):
+    from synth.streams import make_cadence_workload
+    cfg = CONFIGS[1]
+    spec = make_cadence_workload(cfg, units=200).streams[0]
+    ls = Lockstep(cfg, cfg.index, [spec], layers_checked=[0, 35], n_layers=36, budgets=[2048],
+                  window=cfg.window, tol=BF16_TOL, check_kv_every=97, fused=fused,
+                  **_bounds([spec], 2048))
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    _report(ls, f"cadence cfg1 fused={fused}")
+    assert ls.evictions > 50
+
+
+def test_cadence_varlen_batched(gpu):
+    from synth.streams import make_cadence_workload
+    cfg = CONFIGS[2]
+    w = make_cadence_workload(cfg, n_streams=4, units=90)
+    specs = w.streams
+    offsets = [s.offset % 23 for s in specs]
+    ls = Lockstep(cfg, cfg.index, specs, layers_checked=[35], n_layers=36,
+                  budgets=[s.budget // 8 for s in specs], window=cfg.window, tol=BF16_TOL,
+                  check_kv_every=53, fused=True, **_bounds(specs, 512))
+    try:
+        ls.run(offsets=offsets)
+    finally:
+        ls.close()
+    _report(ls, "cadence varlen")
+    assert ls.evictions > 20
