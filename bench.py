@@ -23,6 +23,11 @@ one decode step per side-channel token (opening delimiter, transcript tokens,
 closing delimiter), each step a2t_append_attn on every layer, and the budget
 check once per unit (rate = stream unit-steps/s).
 
+--workload sweep: the KV-budget ablation (Table 3) on 15 synthetic ten-minute
+sessions batched in one cache: for budgets unbounded, 8000, 6000, 4000 and 0
+the full hot path over 600 units; End and Peak resident rows per budget and the
+step time (rate = stream unit-steps/s at budget 4000).
+
 --workload copy: a plain device-to-device copy of 1 GiB (torch's copy
 kernel), the reference point for scaling the HBM byte counters of a profile
 and for the bandwidth a streaming kernel can reach on this device.
@@ -67,6 +72,8 @@ METRICS = {
                "decode-steps/s"),
     "cadence": ("stream unit-steps/s, side-channel cadence (prefill chunk + one decode step "
                 "per transcript token, all layers, eviction per unit)", "unit-steps/s"),
+    "sweep": ("stream unit-steps/s at budget 4000, 15 ten-minute sessions batched (budget sweep "
+              "unbounded/8K/6K/4K/0 reported alongside)", "unit-steps/s"),
     "copy": ("device copy bandwidth (read + write bytes per second)", "GB/s"),
 }
 DEFAULTS = {  # warmup, steps, profile steps
@@ -74,6 +81,7 @@ DEFAULTS = {  # warmup, steps, profile steps
     "varlen": (100, 400, 100),
     "decode": (20, 150, 30),
     "cadence": (200, 100, 30),
+    "sweep": (0, 600, 0),
     "copy": (3, 20, 0),
 }
 
@@ -633,6 +641,82 @@ def run_cadence(args):
     }
 
 
+# ------------------------------------------------------------------- budget sweep
+def run_sweep(args):
+    from synth.streams import make_sessions
+    cfg = CONFIGS[1]
+    n_units = min(args.steps, cfg.units)
+    specs = make_sessions(cfg, range(args.seed, args.seed + 15), units=n_units).streams
+    S, L, Hq, Hkv, D = len(specs), cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    max_n = cfg.max_unit_rows
+    total = max(s.total_rows() for s in specs)
+    keep_rows = max(sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in s.steps) for s in specs)
+    metas = []
+    for u in range(n_units):
+        seg = np.concatenate([s.steps[u].seg for s in specs])
+        pos = np.concatenate([s.steps[u].pos for s in specs])
+        metas.append(((C.c_int32 * S)(*[s.steps[u].n for s in specs]),
+                      (C.c_uint8 * len(seg))(*seg.tolist()), (C.c_int32 * len(pos))(*pos.tolist()),
+                      (C.c_int32 * S)(*[s.steps[u].unit for s in specs])))
+    rows = []
+    value = None
+    last = None
+    for B in (None, 8000, 6000, 4000, 0):
+        r = Runner(cfg, S, total + 64, keep_rows + 64, max_n)
+        torch, lib, h = r.torch, r.lib, r.h
+        if last is None:
+            qp = r.pool((2, L, S * max_n, Hq, D), args.seed)
+            kp = r.pool((2, L, S * max_n, Hkv, D), args.seed + 1)
+            vp = r.pool((2, L, S * max_n, Hkv, D), args.seed + 2)
+            out = torch.empty(S * max_n, Hq, D, dtype=torch.bfloat16, device=r.dev)
+            last = (qp, kp, vp, out)
+        qp, kp, vp, out = last
+        ids = (C.c_int32 * S)(*range(S))
+        budget = (C.c_int32 * S)(*[B or 0] * S)
+        n_ev, unmet = (C.c_int32 * S)(), (C.c_uint8 * S)()
+        sq, skv = S * max_n * Hq * D * 2, S * max_n * Hkv * D * 2
+
+        def run_unit(u):
+            nrows, seg, pos, unit = metas[u]
+            p = u % 2
+            for layer in range(L):
+                oq, okv = (p * L + layer) * sq, (p * L + layer) * skv
+                meta = (seg, pos, unit) if layer == 0 else (None, None, None)
+                r.check(lib.a2t_append_attn(h, layer, S, ids, nrows, kp.data_ptr() + okv,
+                                            vp.data_ptr() + okv, *meta, nrows, qp.data_ptr() + oq,
+                                            out.data_ptr()), "a2t_append_attn")
+            if B is not None:
+                r.check(lib.a2t_evict(h, S, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
+
+        step_ms, total_ms, t_wall, t_enq = r.timed(run_unit, n_units)
+        ends = [r.stream_info(i).resident for i in range(S)]
+        peaks = [r.stream_info(i).peak for i in range(S)]
+        r.close()
+        rows.append({"budget": "unbounded" if B is None else B, "end_rows_mean": float(np.mean(ends)),
+                     "peak_rows_mean": float(np.mean(peaks)), "step_ms_mean": float(step_ms.mean()),
+                     "step_ms_p99": float(np.percentile(step_ms, 99)),
+                     "steps_over_1s": int((step_ms > 1000).sum())})
+        if B == 4000:
+            value = S * n_units / (total_ms * 1e-3)
+            ms_per_step = total_ms / n_units
+    return {
+        "value": value,
+        "ms_per_step": ms_per_step,
+        "config": {
+            "workload": "budget sweep: 15 synthetic ten-minute sessions (600 units of 17 acoustic + "
+                        "2 delimiter + Poisson(3) transcript rows) batched in one cache; budgets "
+                        "unbounded/8000/6000/4000/0 rows, recent window 30 units; 36 layers, 32 "
+                        "query / 8 KV heads, head dim 128, bf16",
+            "sessions": S, "units": n_units,
+            "calls": "a2t_append_attn per layer over all sessions, one a2t_evict per unit",
+            "seed": args.seed,
+        },
+        "sweep": rows,
+        "roofline": None,
+        "cpu_baseline": None,
+    }
+
+
 # ------------------------------------------------------------------- copy reference
 def run_copy(args):
     import torch
@@ -686,10 +770,11 @@ def main():
     args.steps = s if args.steps is None else args.steps
     args.profile_steps = p if args.profile_steps is None else args.profile_steps
     if args.seed is None:
-        args.seed = {"stream": 1, "varlen": 2, "decode": 3, "cadence": 1, "copy": 0}[args.workload]
+        args.seed = {"stream": 1, "varlen": 2, "decode": 3, "cadence": 1, "sweep": 1,
+                     "copy": 0}[args.workload]
 
     res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode,
-           "cadence": run_cadence, "copy": run_copy}[args.workload](args)
+           "cadence": run_cadence, "sweep": run_sweep, "copy": run_copy}[args.workload](args)
     metric, unit = METRICS[args.workload]
     result = {
         "metric": metric,

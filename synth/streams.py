@@ -212,6 +212,20 @@ def make_workload(cfg: WorkloadConfig | int, seed: Optional[int] = None,
     return Workload(config=cfg, seed=seed, streams=streams)
 
 
+def make_sessions(cfg: WorkloadConfig | int, seeds: Sequence[int],
+                  units: Optional[int] = None) -> Workload:
+    """Independent single-stream sessions, one per seed (stream i is the first
+    stream of ``make_workload(cfg, seed=seeds[i])``), batched as one workload:
+    the budget sweep of the ablation runs several sessions per budget."""
+    if isinstance(cfg, int):
+        cfg = CONFIGS[cfg]
+    streams = []
+    for i, sd in enumerate(seeds):
+        st = make_workload(cfg, seed=sd, units=units, n_streams=1).streams[0]
+        streams.append(StreamSpec(stream=i, budget=st.budget, offset=0, steps=st.steps))
+    return Workload(config=cfg, seed=int(seeds[0]) if len(seeds) else 0, streams=streams)
+
+
 CADENCE_KEY_STRIDE = 80   # value keys of unit u's steps: u * 80 + 0 .. 66
 
 

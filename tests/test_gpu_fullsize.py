@@ -103,3 +103,32 @@ def test_config4_full_hour_long_with_control(gpu):
     reduction = 1.0 - peaks[True] / peaks[False]
     print(f"[cfg4 full] peak reduction {reduction:.3f}", flush=True)
     assert reduction > 0.8
+
+
+def test_budget_sweep_fifteen_ten_minute_sessions(gpu):
+    # the KV-budget ablation (Table 3) at full size: 15 ten-minute sessions batched,
+    # budgets unbounded / 8K / 6K / 4K / 0; End and Peak of every session are the
+    # library's and must equal the oracle's replay (checked with every eviction)
+    from synth.streams import make_sessions
+    cfg = CONFIGS[1]
+    specs = make_sessions(cfg, range(1, 16)).streams
+    total = max(s.total_rows() for s in specs)
+    kept = max(row_bounds(s)[1] for s in specs) + 64
+    res = {}
+    for B in (None, 8000, 6000, 4000, 0):
+        run = SampledBatch(cfg, 1, specs, sampled=[], layers_checked=[0],
+                           budgets=[B if B is not None else 0] * len(specs), window=cfg.window,
+                           unit_rows=total + 64, kept_rows=kept, max_step=cfg.max_unit_rows,
+                           tol=BF16_TOL, check_steps=set(), listen_call="fill",
+                           evict=B is not None, label=f"sweep B={B}")
+        try:
+            run.run(progress_every=0)
+            ends = [tr.steps[-1].n_post for tr in run.traces]
+            peaks = [tr.peak for tr in run.traces]
+        finally:
+            run.close()
+        res[B] = (float(np.mean(ends)), float(np.mean(peaks)))
+        print(f"[sweep] budget {B}: End {res[B][0]:.1f} Peak {res[B][1]:.1f}", flush=True)
+    for B in (8000, 6000, 4000):
+        assert B - 19 < res[B][0] <= B < res[B][1] <= B + cfg.max_unit_rows
+    assert res[None][0] == res[None][1] > res[8000][1] > res[6000][1] > res[4000][1] > res[0][1]

@@ -17,7 +17,7 @@ import pytest
 
 from oracle.cache import OracleCache
 from oracle.policy import EVICTABLE_SEGS, compaction_indices, plan_eviction
-from synth.streams import (SEG_ACOUSTIC, SEG_DELIM, SEG_PREFIX, SEG_RESPONSE, SEG_TEXT)
+from synth.streams import (CONFIGS, SEG_ACOUSTIC, SEG_DELIM, SEG_PREFIX, SEG_RESPONSE, SEG_TEXT)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "eviction_worked_examples.json")
 
@@ -254,3 +254,34 @@ def _mutant(window_shift=0, trigger_ge=False, newest_first=False, evict_text=Fal
                                 dict(newest_first=True), dict(evict_text=True)])
 def test_planted_policy_mistakes_fail_the_golden(kw):
     assert _run_golden(_mutant(**kw)) != []
+
+
+def test_budget_sweep_like_table3():
+    # the KV-budget ablation (Table 3) on 15 synthetic ten-minute sessions: with a
+    # feasible budget B the final residency sits just under B and the peak just over
+    # it (at most one unit above); without eviction both equal the session's rows;
+    # the floor keeps only transcript rows plus the recent window
+    from synth.streams import make_sessions
+    from oracle.replay import replay_metadata
+    cfg = CONFIGS[1]
+    w = make_sessions(cfg, range(1, 16))
+    max_unit = cfg.max_unit_rows
+    prev_end = None
+    for B in (None, 8000, 6000, 4000, 0):
+        ends, peaks = [], []
+        for s in w.streams:
+            tr = replay_metadata(s, 10 ** 9 if B is None else B, cfg.window, evict=B is not None)
+            ends.append(tr.steps[-1].n_post)
+            peaks.append(tr.peak)
+            if B is None:
+                assert ends[-1] == peaks[-1] == s.total_rows()
+            elif B > 0:
+                assert B - 19 < ends[-1] <= B < peaks[-1] <= B + max_unit
+            else:
+                text = sum(int(np.sum(st.seg == 3)) for st in s.steps)
+                last = sum(st.n for st in s.steps[-cfg.window:])
+                last_text = sum(int(np.sum(st.seg == 3)) for st in s.steps[-cfg.window:])
+                assert ends[-1] == text - last_text + last
+        if prev_end is not None:
+            assert np.mean(ends) < prev_end
+        prev_end = np.mean(ends)
