@@ -1,0 +1,117 @@
+"""The adaptation objective of Sec. 3.2 on given logits (oracle; test infrastructure only).
+
+Plain float64 numpy, written from the definitions: student logits cover the
+extended vocabulary (the teacher's V tokens plus the added side-channel
+tokens); the teacher's distribution over V is extended with zero probability
+on the added tokens.  Rows are prediction positions:
+
+* kind 1 -- a transcription token or delimiter: masked cross-entropy against
+  its target (L_ASR is the mean over these rows);
+* kind 2 -- a native prediction position aligned with the teacher: the
+  divergence T^2 KL(P_T || P_S) at temperature T (L_native is its mean over
+  these rows);
+* kind 0 -- neither (no loss).
+
+L_dec groups the native rows that are a unit's first decision by the token fed
+(listen / speak / other; ``dec_group`` 0 / 1 / 2, -1 for the rest), L_turn the
+native non-decision rows by whether the fed token ends the turn (``turn_group``
+1 / 0, -1 for the rest); each averages the same per-row divergences within a
+group and then over the groups present.  L is the sum of the four terms (unit
+weights).  The gradient with respect to the student logits is given for the
+fused kernel's second output.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict
+
+import numpy as np
+
+KIND_NONE, KIND_ASR, KIND_NATIVE = 0, 1, 2
+N_DEC_GROUPS, N_TURN_GROUPS = 3, 2
+
+
+def log_softmax(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, np.float64)
+    m = np.max(x, axis=-1, keepdims=True)
+    return x - m - np.log(np.sum(np.exp(x - m), axis=-1, keepdims=True))
+
+
+@dataclass
+class DistillResult:
+    losses: Dict[str, float]      # asr, native, dec, turn, total
+    ce: np.ndarray                # [N] per-row cross-entropy (0 where not ASR)
+    kl: np.ndarray                # [N] per-row T^2 KL (0 where not native)
+    grad: np.ndarray              # [N][V + added] dL / d student logits
+
+
+def row_weights(kind, dec_group, turn_group):
+    """Per-row coefficients of the four means: ce weight and kl weight."""
+    kind = np.asarray(kind)
+    dec_group = np.asarray(dec_group)
+    turn_group = np.asarray(turn_group)
+    n = kind.shape[0]
+    w_ce = np.zeros(n)
+    w_kl = np.zeros(n)
+    asr = kind == KIND_ASR
+    nat = kind == KIND_NATIVE
+    if asr.any():
+        w_ce[asr] = 1.0 / asr.sum()
+    if nat.any():
+        w_kl[nat] += 1.0 / nat.sum()
+    for groups, n_groups in ((dec_group, N_DEC_GROUPS), (turn_group, N_TURN_GROUPS)):
+        members = [nat & (groups == g) for g in range(n_groups)]
+        present = [m for m in members if m.any()]
+        for m in present:
+            w_kl[m] += 1.0 / (len(present) * m.sum())
+    return w_ce, w_kl
+
+
+def distill_losses(student, teacher, kind, target, dec_group, turn_group,
+                   temperature: float = 1.0) -> DistillResult:
+    s = np.asarray(student, np.float64)
+    t = np.asarray(teacher, np.float64)
+    kind = np.asarray(kind)
+    target = np.asarray(target)
+    dec_group = np.asarray(dec_group)
+    turn_group = np.asarray(turn_group)
+    n, vs = s.shape
+    v = t.shape[1]
+    T = float(temperature)
+    # teacher over the extended vocabulary: zero probability on the added tokens
+    p_t = np.zeros((n, vs))
+    p_t[:, :v] = np.exp(log_softmax(t / T))
+    logp_sT = log_softmax(s / T)
+    logp_s1 = log_softmax(s)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        terms = np.where(p_t > 0, p_t * (np.log(np.where(p_t > 0, p_t, 1.0)) - logp_sT), 0.0)
+    kl = (T * T) * terms.sum(axis=1)
+    ce = np.zeros(n)
+    asr = kind == KIND_ASR
+    ce[asr] = -logp_s1[np.flatnonzero(asr), target[asr]]
+    kl = np.where(kind == KIND_NATIVE, kl, 0.0)
+
+    nat = kind == KIND_NATIVE
+    l_asr = float(ce[asr].mean()) if asr.any() else 0.0
+    l_nat = float(kl[nat].mean()) if nat.any() else 0.0
+
+    def balanced(groups, n_groups):
+        means = [kl[nat & (groups == g)].mean() for g in range(n_groups)
+                 if (nat & (groups == g)).any()]
+        return float(np.mean(means)) if means else 0.0
+
+    l_dec = balanced(dec_group, N_DEC_GROUPS)
+    l_turn = balanced(turn_group, N_TURN_GROUPS)
+
+    w_ce, w_kl = row_weights(kind, dec_group, turn_group)
+    grad = np.zeros((n, vs))
+    p_s1 = np.exp(logp_s1)
+    p_sT = np.exp(logp_sT)
+    # d/ds of T^2 KL(p_t || softmax(s/T)) = T (softmax(s/T) - p_t)
+    grad += (w_kl * T)[:, None] * (p_sT - p_t)
+    onehot = np.zeros((n, vs))
+    onehot[np.flatnonzero(asr), target[asr]] = 1.0
+    grad += w_ce[:, None] * (p_s1 - onehot)
+    losses = {"asr": l_asr, "native": l_nat, "dec": l_dec, "turn": l_turn,
+              "total": l_asr + l_nat + l_dec + l_turn}
+    return DistillResult(losses=losses, ce=ce, kl=kl, grad=grad)
