@@ -28,6 +28,11 @@ sessions batched in one cache: for budgets unbounded, 8000, 6000, 4000 and 0
 the full hot path over 600 units; End and Peak resident rows per budget and the
 step time (rate = stream unit-steps/s at budget 4000).
 
+--workload distill: the adaptation objective (Sec. 3.2) on a batch of 16
+short utterances x 12 units (~1,340 prediction rows) over a vocabulary of
+151,936 teacher tokens + 2 added tokens, bf16 logits: losses and the gradient
+with respect to the student logits per evaluation (rate = evaluations/s).
+
 --workload copy: a plain device-to-device copy of 1 GiB (torch's copy
 kernel), the reference point for scaling the HBM byte counters of a profile
 and for the bandwidth a streaming kernel can reach on this device.
@@ -74,6 +79,8 @@ METRICS = {
                 "per transcript token, all layers, eviction per unit)", "unit-steps/s"),
     "sweep": ("stream unit-steps/s at budget 4000, 15 ten-minute sessions batched (budget sweep "
               "unbounded/8K/6K/4K/0 reported alongside)", "unit-steps/s"),
+    "distill": ("objective evaluations/s (masked CE + T^2 KL + group-balanced means and the "
+                "student-logit gradient over a 16-utterance batch)", "evaluations/s"),
     "copy": ("device copy bandwidth (read + write bytes per second)", "GB/s"),
 }
 DEFAULTS = {  # warmup, steps, profile steps
@@ -82,6 +89,7 @@ DEFAULTS = {  # warmup, steps, profile steps
     "decode": (20, 150, 30),
     "cadence": (200, 100, 30),
     "sweep": (0, 600, 0),
+    "distill": (5, 40, 20),
     "copy": (3, 20, 0),
 }
 
@@ -717,6 +725,101 @@ def run_sweep(args):
     }
 
 
+# ------------------------------------------------------------------- adaptation objective
+def run_distill(args):
+    import torch
+    import paper_2609_31224_amd as a2t
+    from synth.distill import make_distill_batch
+    vocab, added = 151936, 2
+    b = make_distill_batch(seed=args.seed, n_utt=16, units=12, vocab=vocab, added=added,
+                           dtype="bf16")
+    n = b.n
+    ss = (vocab + added + 7) // 8 * 8
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    st = torch.zeros(n, ss, dtype=torch.bfloat16, device=dev)
+    st[:, :vocab + added] = torch.from_numpy(b.student).to(dev).to(torch.bfloat16)
+    te = torch.from_numpy(b.teacher).to(dev).to(torch.bfloat16).contiguous()
+    grad = torch.empty_like(st)
+    losses = torch.zeros(5, dtype=torch.float32, device=dev)
+    d = a2t.a2t_distill_create(n, vocab, added, a2t.A2T_BF16, stream=stream)
+    lib = a2t.raw_lib()
+    P8, P32 = C.POINTER(C.c_int8), C.POINTER(C.c_int32)
+    kind = np.ascontiguousarray(b.kind, np.int8)
+    tgt = np.ascontiguousarray(b.target, np.int32)
+    dec = np.ascontiguousarray(b.dec_group, np.int8)
+    turn = np.ascontiguousarray(b.turn_group, np.int8)
+
+    def call(with_grad=True):
+        rc = lib.a2t_distill_loss(d.ptr, n, st.data_ptr(), ss, te.data_ptr(), vocab,
+                                  kind.ctypes.data_as(P8), tgt.ctypes.data_as(P32),
+                                  dec.ctypes.data_as(P8), turn.ctypes.data_as(P8), 1.0,
+                                  losses.data_ptr(), grad.data_ptr() if with_grad else None)
+        if rc:
+            raise a2t.A2TError(rc, "a2t_distill_loss")
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for j in range(args.steps):
+        call()
+        evs[j + 1].record(stream)
+    torch.cuda.synchronize()
+    step_ms = np.array([evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps)])
+    total_ms = float(evs[0].elapsed_time(evs[-1]))
+    kern = {}
+    for name, wg in (("distill_row", True), ("distill_row_loss_only", False)):
+        lib.a2t_distill_profile_enable(d.ptr, 1)
+        for _ in range(max(1, args.profile_steps)):
+            call(wg)
+        nl, ms = C.c_int64(), C.c_double()
+        lib.a2t_distill_kernel_time(d.ptr, C.byref(nl), C.byref(ms))
+        lib.a2t_distill_profile_enable(d.ptr, 0)
+        kern[name] = {"launches": nl.value, "avg_us": ms.value * 1e3 / max(1, nl.value)}
+    a2t.a2t_distill_destroy(d)
+    # algorithmic bytes of one evaluation: read both logit rows once, write the gradient once
+    alg = n * ((vocab + added) * 2 + vocab * 2 + (vocab + added) * 2)
+    alg_loss = n * ((vocab + added) * 2 + vocab * 2)
+    us = kern["distill_row"]["avg_us"]
+    achieved = alg / (us * 1e-6) / 1e9
+    base_line = None
+    if not args.no_cpu_baseline:
+        from oracle.distill import row_terms, row_gradient
+        rows = np.arange(0, n, max(1, n // 48))[:48]
+        t0 = time.perf_counter()
+        row_terms(b.student[rows], b.teacher[rows], np.where(b.kind[rows] == 1, b.target[rows], -1))
+        row_gradient(b.student[rows], b.teacher[rows], np.where(b.kind[rows] == 1, b.target[rows], -1),
+                     np.ones(len(rows)), np.ones(len(rows)))
+        dt = time.perf_counter() - t0
+        base_line = {"value": len(rows) / dt / n, "unit": "evaluations/s", "cores": _threads_used(),
+                     "kind": "oracle",
+                     "sample": f"{len(rows)} of {n} rows (per-row terms and gradient, fp64 numpy), "
+                               f"scaled to the batch; {dt:.1f} s of CPU work"}
+    return {
+        "value": 1000.0 * args.steps / total_ms,
+        "ms_per_step": total_ms / args.steps,
+        "config": {
+            "workload": f"adaptation objective: 16 utterances x 12 units = {n} prediction rows "
+                        f"(first decisions, side-channel tokens, native non-decision rows), vocabulary "
+                        f"{vocab} + {added} added tokens, bf16 logits, T = 1, losses + gradient",
+            "rows": n, "seed": args.seed,
+        },
+        "roofline": {"bound": "hbm", "kernel": "distill_row", "achieved": achieved,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": None, "avg_launch_us": us, "alg_bytes_per_launch": alg},
+        "loss_only": {"avg_launch_us": kern["distill_row_loss_only"]["avg_us"],
+                      "alg_bytes_per_launch": alg_loss,
+                      "achieved_gbps": alg_loss / (kern["distill_row_loss_only"]["avg_us"] * 1e-6) / 1e9},
+        "kernels_us": kern,
+        "unit_ms": {"mean": float(step_ms.mean()), "p50": float(np.percentile(step_ms, 50)),
+                    "p99": float(np.percentile(step_ms, 99))},
+        "cpu_baseline": base_line,
+    }
+
+
 # ------------------------------------------------------------------- copy reference
 def run_copy(args):
     import torch
@@ -771,10 +874,11 @@ def main():
     args.profile_steps = p if args.profile_steps is None else args.profile_steps
     if args.seed is None:
         args.seed = {"stream": 1, "varlen": 2, "decode": 3, "cadence": 1, "sweep": 1,
-                     "copy": 0}[args.workload]
+                     "distill": 14, "copy": 0}[args.workload]
 
     res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode,
-           "cadence": run_cadence, "sweep": run_sweep, "copy": run_copy}[args.workload](args)
+           "cadence": run_cadence, "sweep": run_sweep, "distill": run_distill,
+           "copy": run_copy}[args.workload](args)
     metric, unit = METRICS[args.workload]
     result = {
         "metric": metric,

@@ -259,6 +259,68 @@ int a2t_kernel_time(a2t_cache* c, const char* kernel, int64_t* launches, double*
 const char* a2t_status_str(int status);
 int a2t_abi_version(void);
 
+/* ---------------------------------------------------------------------------
+ * Adaptation objective (Sec. 3.2): the training loss that teaches the side
+ * channel while keeping native behaviour, on given logits.
+ *
+ *   L = L_ASR + L_native + L_dec + L_turn (unit weights)
+ *
+ * Rows are prediction positions.  Student logits cover the extended vocabulary
+ * (the teacher's `vocab` tokens followed by `n_added` added tokens); the
+ * teacher's distribution over `vocab` is extended with zero probability on the
+ * added tokens.  Per row, `kind`:
+ *   A2T_ROW_ASR     a transcription token or delimiter: cross-entropy of the
+ *                   student (temperature 1) against `target`; L_ASR is the mean
+ *                   over these rows;
+ *   A2T_ROW_NATIVE  a native prediction position aligned with the teacher:
+ *                   T^2 KL(P_T || P_S) at temperature T; L_native is the mean
+ *                   over these rows;
+ *   A2T_ROW_NONE    no loss, zero gradient.
+ * L_dec averages the native rows' divergences within each decision group
+ * (`dec_group` 0 listen, 1 speak, 2 other; -1 not a unit's first decision) and
+ * then over the groups present; L_turn does the same over `turn_group`
+ * (1 turn end, 0 continuation, -1 none).
+ * ------------------------------------------------------------------------- */
+#define A2T_ROW_NONE 0
+#define A2T_ROW_ASR 1
+#define A2T_ROW_NATIVE 2
+
+typedef struct a2t_distill a2t_distill;
+
+/* Scratch for up to max_rows rows per call (per-row losses and weights, a
+ * pinned staging area); the only allocating calls.  dtype: A2T_F32 or
+ * A2T_BF16 for logits and gradient.  hip_stream: as for a2t_cache_create.
+ * Errors: INVALID (sizes < 1, n_added < 0, dtype), OOM, HIP, NODEV. */
+int a2t_distill_create(int32_t max_rows, int32_t vocab, int32_t n_added, int32_t dtype,
+                       int32_t device, void* hip_stream, a2t_distill** out);
+int a2t_distill_destroy(a2t_distill* d);
+
+/* One evaluation over n_rows rows, asynchronous on the handle's stream.
+ *   student         device [n_rows][student_stride], vocab + n_added logits per row
+ *   teacher         device [n_rows][teacher_stride], vocab logits per row
+ *                   (strides in elements, multiples of 8; pointers 16-byte aligned)
+ *   kind, target, dec_group, turn_group
+ *                   host [n_rows]; target in [0, vocab + n_added) on ASR rows
+ *   temperature     T > 0 of the divergence (the paper uses 1)
+ *   losses          device float[5] out: L_ASR, L_native, L_dec, L_turn, L
+ *   grad            device [n_rows][student_stride] out, dL/d student logits in
+ *                   the logits dtype, or NULL (loss only)
+ * Host arrays are consumed before the call returns; device buffers must stay
+ * valid until the stream reaches the work.  Errors: INVALID (n_rows out of
+ * [1, max_rows], strides, alignment, kinds, groups, targets, T), HIP. */
+int a2t_distill_loss(a2t_distill* d, int32_t n_rows, const void* student, int64_t student_stride,
+                     const void* teacher, int64_t teacher_stride, const int8_t* kind,
+                     const int32_t* target, const int8_t* dec_group, const int8_t* turn_group,
+                     float temperature, float* losses, void* grad);
+
+/* Timing of the per-row kernel (for benchmarks): with enable != 0 every later
+ * a2t_distill_loss records start/stop events at that dispatch's own begin and
+ * end; a2t_distill_kernel_time waits for them and reports the number of
+ * timed launches and their summed duration in milliseconds since the last
+ * report.  Errors: INVALID, HIP. */
+int a2t_distill_profile_enable(a2t_distill* d, int32_t enable);
+int a2t_distill_kernel_time(a2t_distill* d, int64_t* launches, double* total_ms);
+
 #ifdef __cplusplus
 }
 #endif

@@ -67,31 +67,57 @@ def row_weights(kind, dec_group, turn_group):
     return w_ce, w_kl
 
 
-def distill_losses(student, teacher, kind, target, dec_group, turn_group,
-                   temperature: float = 1.0) -> DistillResult:
+def row_terms(student, teacher, target, temperature: float = 1.0):
+    """Per-row cross-entropy (temperature 1) against ``target`` (rows with a
+    negative target get 0) and T^2 KL(P_T || P_S) at temperature T, for every
+    row given; student [n][V + added], teacher [n][V]."""
     s = np.asarray(student, np.float64)
     t = np.asarray(teacher, np.float64)
+    target = np.asarray(target)
+    n, vs = s.shape
+    v = t.shape[1]
+    T = float(temperature)
+    logp_t = log_softmax(t / T)
+    logp_sT = log_softmax(s / T)
+    # the added tokens have zero teacher probability and contribute nothing
+    kl = (T * T) * np.sum(np.exp(logp_t) * (logp_t - logp_sT[:, :v]), axis=1)
+    logp_s1 = log_softmax(s)
+    ce = np.zeros(n)
+    has = target >= 0
+    ce[has] = -logp_s1[np.flatnonzero(has), target[has]]
+    return ce, kl
+
+
+def row_gradient(student, teacher, target, w_ce, w_kl, temperature: float = 1.0):
+    """dL/d student logits of the given rows with their coefficients:
+    w_kl T (softmax(s/T) - P_T extended) + w_ce (softmax(s) - onehot(target))."""
+    s = np.asarray(student, np.float64)
+    t = np.asarray(teacher, np.float64)
+    target = np.asarray(target)
+    n, vs = s.shape
+    v = t.shape[1]
+    T = float(temperature)
+    p_t = np.zeros((n, vs))
+    p_t[:, :v] = np.exp(log_softmax(t / T))
+    grad = (np.asarray(w_kl, np.float64) * T)[:, None] * (np.exp(log_softmax(s / T)) - p_t)
+    onehot = np.zeros((n, vs))
+    has = target >= 0
+    onehot[np.flatnonzero(has), target[has]] = 1.0
+    grad += np.asarray(w_ce, np.float64)[:, None] * (np.exp(log_softmax(s)) - onehot)
+    return grad
+
+
+def distill_losses(student, teacher, kind, target, dec_group, turn_group,
+                   temperature: float = 1.0) -> DistillResult:
     kind = np.asarray(kind)
     target = np.asarray(target)
     dec_group = np.asarray(dec_group)
     turn_group = np.asarray(turn_group)
-    n, vs = s.shape
-    v = t.shape[1]
-    T = float(temperature)
-    # teacher over the extended vocabulary: zero probability on the added tokens
-    p_t = np.zeros((n, vs))
-    p_t[:, :v] = np.exp(log_softmax(t / T))
-    logp_sT = log_softmax(s / T)
-    logp_s1 = log_softmax(s)
-    with np.errstate(divide="ignore", invalid="ignore"):
-        terms = np.where(p_t > 0, p_t * (np.log(np.where(p_t > 0, p_t, 1.0)) - logp_sT), 0.0)
-    kl = (T * T) * terms.sum(axis=1)
-    ce = np.zeros(n)
     asr = kind == KIND_ASR
-    ce[asr] = -logp_s1[np.flatnonzero(asr), target[asr]]
-    kl = np.where(kind == KIND_NATIVE, kl, 0.0)
-
     nat = kind == KIND_NATIVE
+    ce, kl = row_terms(student, teacher, np.where(asr, target, -1), temperature)
+    kl = np.where(nat, kl, 0.0)
+
     l_asr = float(ce[asr].mean()) if asr.any() else 0.0
     l_nat = float(kl[nat].mean()) if nat.any() else 0.0
 
@@ -102,16 +128,8 @@ def distill_losses(student, teacher, kind, target, dec_group, turn_group,
 
     l_dec = balanced(dec_group, N_DEC_GROUPS)
     l_turn = balanced(turn_group, N_TURN_GROUPS)
-
     w_ce, w_kl = row_weights(kind, dec_group, turn_group)
-    grad = np.zeros((n, vs))
-    p_s1 = np.exp(logp_s1)
-    p_sT = np.exp(logp_sT)
-    # d/ds of T^2 KL(p_t || softmax(s/T)) = T (softmax(s/T) - p_t)
-    grad += (w_kl * T)[:, None] * (p_sT - p_t)
-    onehot = np.zeros((n, vs))
-    onehot[np.flatnonzero(asr), target[asr]] = 1.0
-    grad += w_ce[:, None] * (p_s1 - onehot)
+    grad = row_gradient(student, teacher, np.where(asr, target, -1), w_ce, w_kl, temperature)
     losses = {"asr": l_asr, "native": l_nat, "dec": l_dec, "turn": l_turn,
               "total": l_asr + l_nat + l_dec + l_turn}
     return DistillResult(losses=losses, ce=ce, kl=kl, grad=grad)

@@ -38,7 +38,10 @@ EXPORTED = (
     "a2t_chunk_attn", "a2t_append_attn", "a2t_decode_attn", "a2t_evict", "a2t_stream_info_get",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
     "a2t_profile_enable", "a2t_kernel_time", "a2t_status_str", "a2t_abi_version",
+    "a2t_distill_create", "a2t_distill_destroy", "a2t_distill_loss",
+    "a2t_distill_profile_enable", "a2t_distill_kernel_time",
 )
+A2T_ROW_NONE, A2T_ROW_ASR, A2T_ROW_NATIVE = 0, 1, 2
 
 
 class a2t_config(C.Structure):
@@ -92,6 +95,12 @@ def _load():
         "a2t_kernel_time": (C.c_int, [VP, C.c_char_p, P(C.c_int64), P(C.c_double)]),
         "a2t_status_str": (C.c_char_p, [C.c_int]),
         "a2t_abi_version": (C.c_int, []),
+        "a2t_distill_create": (C.c_int, [I32, I32, I32, I32, I32, VP, P(VP)]),
+        "a2t_distill_destroy": (C.c_int, [VP]),
+        "a2t_distill_loss": (C.c_int, [VP, I32, VP, C.c_int64, VP, C.c_int64, P(C.c_int8), P(I32),
+                                       P(C.c_int8), P(C.c_int8), C.c_float, VP, VP]),
+        "a2t_distill_profile_enable": (C.c_int, [VP, I32]),
+        "a2t_distill_kernel_time": (C.c_int, [VP, P(C.c_int64), P(C.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -315,3 +324,48 @@ def raw_lib():
     """The ctypes library with argument types set, for callers that marshal
     their arguments once and call the C entry points directly."""
     return _lib
+
+
+# ---- adaptation objective (Sec. 3.2)
+@dataclass
+class Distill:
+    """Handle returned by a2t_distill_create."""
+    ptr: C.c_void_p
+    max_rows: int
+    vocab: int
+    n_added: int
+    dtype: int
+
+
+def a2t_distill_create(max_rows: int, vocab: int, n_added: int, dtype: int, device: int = 0,
+                       stream=None) -> Distill:
+    out = C.c_void_p()
+    _check(_lib.a2t_distill_create(max_rows, vocab, n_added, dtype, device, _stream_handle(stream),
+                                   C.byref(out)), "a2t_distill_create")
+    return Distill(out, max_rows, vocab, n_added, dtype)
+
+
+def a2t_distill_destroy(d: Distill) -> None:
+    _check(_lib.a2t_distill_destroy(d.ptr), "a2t_distill_destroy")
+
+
+def a2t_distill_loss(d: Distill, student, teacher, kind, target, dec_group, turn_group,
+                     temperature: float, losses, grad=None) -> None:
+    """student / teacher / grad: GPU tensors [n_rows][stride] (rows of the
+    extended / teacher vocabulary, strides multiples of 8); kind, target,
+    dec_group, turn_group: host arrays [n_rows]; losses: GPU float32 [5]."""
+    import torch
+    dt = torch.float32 if d.dtype == A2T_F32 else torch.bfloat16
+    n = int(student.shape[0])
+    kd = np.ascontiguousarray(np.asarray(kind), dtype=np.int8)
+    tg = _i32(target)
+    dg = np.ascontiguousarray(np.asarray(dec_group), dtype=np.int8)
+    tu = np.ascontiguousarray(np.asarray(turn_group), dtype=np.int8)
+    if not (kd.shape == tg.shape == dg.shape == tu.shape == (n,)):
+        raise ValueError("row metadata must have one entry per row")
+    rc = _lib.a2t_distill_loss(d.ptr, n, _dev(student, "student", dt), int(student.stride(0)),
+                               _dev(teacher, "teacher", dt), int(teacher.stride(0)),
+                               _p(kd, C.c_int8), _p(tg, C.c_int32), _p(dg, C.c_int8),
+                               _p(tu, C.c_int8), float(temperature),
+                               _dev(losses, "losses", torch.float32), _dev(grad, "grad", dt))
+    _check(rc, "a2t_distill_loss")
