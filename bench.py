@@ -857,8 +857,8 @@ def main():
                     help="extra steps with every dispatch timestamped (roofline)")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-units", type=int, default=6)
-    ap.add_argument("--cpu-sample-layers", type=int, default=4)
+    ap.add_argument("--cpu-sample-units", type=int, default=64)
+    ap.add_argument("--cpu-sample-layers", type=int, default=8)
     ap.add_argument("--unfused", action="store_true",
                     help="stream workload: per layer a2t_append then a2t_chunk_attn")
     ap.add_argument("--decode-call", choices=("decode", "fused"), default="decode",

@@ -487,6 +487,10 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
     // DMAs write LDS only, so the two paths need not share registers: the fast
     // path is a scalar tile base plus 32-bit lane offsets
     auto issue = [&](int t, TileBuf<D>& buf) {
+        // opaque tile index: the prologue's issues sit in the query-pass loop, and
+        // hoisted out of it their general-path addresses would be computed
+        // unconditionally
+        asm volatile("" : "+s"(t));
         const int kb = t * kTileKeys;
         bool in_kept = false;
         const int fb = fast_base(kb, &in_kept);
@@ -506,6 +510,9 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                 dma16(src_of(vk, vu, v_in, kb + pr, pc ^ (2 * (pr & (CPR / 2 - 1)))),
                       &buf.v[(w * OPS + i) * 512]);
             }
+            // keeps the two paths' DMAs apart: merged into one, they would
+            // compute the general path's per-lane addresses for every tile
+            asm volatile("" ::: "memory");
         }
     };
     // a tile index past the range issues the same number of DMAs, all lanes
@@ -774,12 +781,12 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 
 // ----------------------------------------------------------------- attn_merge
 // grid (row blocks, kv head, stream); each thread owns 4 output elements of
-// one query row.  The splits are read 16 at a time (all loads of a batch in
+// one query row.  The splits are read 32 at a time (all loads of a batch in
 // flight together) and combined in fixed split order, so the result is
 // deterministic.
 template <typename T, class BT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
-    constexpr int B = 16;
+    constexpr int B = 32;
     const AttnDesc d = b.d[blockIdx.z];
     if (d.splits <= 1) return;
     const int G = st.Hq / st.Hkv, M = G * d.n_q, D = st.D, g = blockIdx.y;
