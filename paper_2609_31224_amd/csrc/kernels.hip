@@ -583,9 +583,11 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
         const bool active = mw < M;
         const int mq = mw + l16;
 
-        // load order: tile t0, Q, tiles t0+1 and t0+2 (compiler barriers keep
-        // it), so the Q latency overlaps tile t0's and waiting for Q leaves the
-        // next two tiles in flight
+        // load order: tile t0 and Q, then tiles t0+1 and t0+2 once Q is rotated
+        // (compiler barriers keep it).  Every workgroup of a launch starts at
+        // once; asking for only one tile first lets the first tiles arrive
+        // early instead of behind all of the launch's bytes, so the first
+        // tile's compute overlaps the transfer of the next two.
         if (t0 < t1) issue(t0, ring[0]);
         asm volatile("" ::: "memory");
         // unconditional loads (rows past M read row M-1 and are zeroed below): a
@@ -605,8 +607,6 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                 for (int e2 = 0; e2 < 4; ++e2) cs[s][e2] = cs4[(32 * s + 8 * lg) / 2 + e2];
         }
         asm volatile("" ::: "memory");
-        issue_or_dummy(t0 + 1, ring[1]);
-        issue_or_dummy(t0 + 2, ring[2]);
 
         // Q^T operand: rotated, scaled by scale*log2(e), bf16
         bf16x8 qop[KS];
@@ -640,6 +640,10 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                                        pack_bf16x2(x[s][4], x[s][5]), pack_bf16x2(x[s][6], x[s][7])));
         }
 
+        // after the rotation, which waited for Q (and so for tile t0)
+        asm volatile("" :: "v"(qop[0]), "v"(qop[KS - 1]) : "memory");
+        issue_or_dummy(t0 + 1, ring[1]);
+        issue_or_dummy(t0 + 2, ring[2]);
         uint32_t vtr_off[DB];
         {
             const int r0 = 4 * lg + (l16 >> 2);  // rows 32c + r0 and +16 share r0's swizzle
@@ -763,15 +767,19 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                         make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
                 }
             } else {
+                // split partials are read once, by the merge launch: non-temporal
+                // stores send them on to memory now instead of leaving dirty L2
+                // lines for the end-of-kernel write-back
                 float* po = st.ws + d.ws_off;
                 float* prow = po + (((int64_t)sp * st.Hkv + g) * M + mq) * D;
 #pragma unroll
                 for (int db = 0; db < DB; ++db)
-                    *reinterpret_cast<f32x4*>(prow + db * 16 + 4 * lg) = acc[db];
+                    __builtin_nontemporal_store(acc[db], reinterpret_cast<f32x4*>(prow + db * 16 + 4 * lg));
                 if (lg == 0) {
                     float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
-                    *reinterpret_cast<float2*>(pml + (((int64_t)sp * st.Hkv + g) * M + mq) * 2) =
-                        make_float2(mrun, lrun);
+                    float* mp = pml + (((int64_t)sp * st.Hkv + g) * M + mq) * 2;
+                    __builtin_nontemporal_store(mrun, mp);
+                    __builtin_nontemporal_store(lrun, mp + 1);
                 }
             }
         }
