@@ -90,6 +90,11 @@ struct a2t_cache {
     // attention tuning
     int target_wgs = 1024;
     int force_splits = 0;
+    // the last split plan (every layer of a step plans the same resident counts)
+    int plan_n = 0;
+    int plan_force = -1;
+    std::vector<int> plan_tiles, plan_splits, plan_tmp, plan_order;
+    std::vector<int64_t> plan_heap;
     bool force_valu = false;
     // profiling
     bool prof_on = false;
@@ -213,33 +218,75 @@ int check_streams(a2t_cache* c, int32_t n, const int32_t* ids) {
 bool is_evictable(uint8_t seg) { return seg == A2T_SEG_ACOUSTIC || seg == A2T_SEG_DELIM; }
 
 // Key splits per stream for one attention launch.  A workgroup of the MFMA
-// kernel occupies a whole CU (its LDS ring), so a launch runs in rounds of
-// `slots` (= CU count) workgroups and takes about rounds x (tiles of its
-// largest workgroup + its fixed part).  For each tile budget per workgroup
-// (>= 2 tiles) every stream gets the fewest splits that respect it; the budget
-// with the lowest cost wins (ties: fewer workgroups, i.e. fewer split
+// kernel occupies a whole CU (its LDS ring) and the dispatcher hands the next
+// workgroup to the first CU that frees up, so a launch takes about the makespan
+// of its workgroups dispatched in order over `slots` (= CU count) CUs.  For each
+// tile budget per workgroup (>= 2 tiles) every stream gets the fewest splits that
+// respect it; a workgroup costs its tiles plus a fixed part (first-load latency,
+// partial write: ~2 tiles).  Streams are dispatched longest workgroups first
+// (attn_launch orders the descriptors that way), and the budget with the
+// shortest simulated makespan wins (ties: fewer workgroups, i.e. fewer split
 // partials).  The partials must fit the workspace.
-void plan_splits(const a2t_cache* c, int n, const int* tiles, const int64_t* floats_per_split,
+constexpr int kWgFixedTiles = 2;
+
+int64_t launch_makespan(int n, const int* tiles, const int* splits, int Hkv, int slots,
+                        std::vector<int>& order, std::vector<int64_t>& heap) {
+    int64_t wgs = 0, largest = 0;
+    order.resize(n);
+    for (int i = 0; i < n; ++i) {
+        order[i] = i;
+        wgs += (int64_t)splits[i] * Hkv;
+        largest = std::max<int64_t>(largest, (tiles[i] + splits[i] - 1) / splits[i]);
+    }
+    if (wgs <= slots) return largest + kWgFixedTiles;
+    auto cost = [&](int i) { return (int64_t)(tiles[i] + splits[i] - 1) / splits[i] + kWgFixedTiles; };
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cost(a) > cost(b); });
+    // min-heap of CU finish times
+    heap.assign(slots, 0);
+    auto gt = std::greater<int64_t>();
+    for (int i : order) {
+        const int64_t ci = cost(i);
+        for (int64_t k = 0; k < (int64_t)splits[i] * Hkv; ++k) {
+            std::pop_heap(heap.begin(), heap.end(), gt);
+            heap.back() += ci;
+            std::push_heap(heap.begin(), heap.end(), gt);
+        }
+    }
+    return *std::max_element(heap.begin(), heap.end());
+}
+
+void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_per_split,
                  int* splits) {
+    // every layer of a step plans the same resident counts: reuse the last plan
+    // while its partials fit the workspace (query counts may differ)
+    if (c->plan_n == n && std::equal(tiles, tiles + n, c->plan_tiles.begin()) &&
+        c->plan_force == c->force_splits) {
+        int64_t ws = 0;
+        for (int i = 0; i < n; ++i)
+            if (c->plan_splits[i] > 1) ws += c->plan_splits[i] * floats_per_split[i];
+        if (ws <= c->dev.ws_floats) {
+            std::copy(c->plan_splits.begin(), c->plan_splits.begin() + n, splits);
+            return;
+        }
+    }
+    const int Hkv = c->cfg.n_kv_heads;
     if (c->force_splits <= 0) {
-        const int Hkv = c->cfg.n_kv_heads;
         int max_tiles = 1;
         for (int i = 0; i < n; ++i) max_tiles = std::max(max_tiles, tiles[i]);
         int64_t best_cost = INT64_MAX, best_w = 0;
         int best_budget = max_tiles;
+        std::vector<int>& sp = c->plan_tmp;
+        sp.resize(n);
         for (int budget = 2; budget <= std::max(2, max_tiles); ++budget) {
             int64_t w = 0, ws = 0;
-            int largest = 1;
             for (int i = 0; i < n; ++i) {
-                const int sp = std::max(1, std::min((tiles[i] + budget - 1) / budget, kMaxSplits));
-                w += (int64_t)sp * Hkv;
-                if (sp > 1) ws += sp * floats_per_split[i];
-                largest = std::max(largest, (tiles[i] + sp - 1) / sp);
+                sp[i] = std::max(1, std::min((tiles[i] + budget - 1) / budget, kMaxSplits));
+                w += (int64_t)sp[i] * Hkv;
+                if (sp[i] > 1) ws += sp[i] * floats_per_split[i];
             }
             if (ws > c->dev.ws_floats) continue;
-            // a workgroup's fixed part (first-load latency, partial write) ~ 2 tiles
-            const int64_t rounds = (w + c->target_wgs - 1) / c->target_wgs;
-            const int64_t cost = rounds * (largest + 2);
+            const int64_t cost = launch_makespan(n, tiles, sp.data(), Hkv, c->target_wgs,
+                                                 c->plan_order, c->plan_heap);
             if (cost < best_cost || (cost == best_cost && w < best_w)) {
                 best_cost = cost;
                 best_w = w;
@@ -248,8 +295,15 @@ void plan_splits(const a2t_cache* c, int n, const int* tiles, const int64_t* flo
         }
         for (int i = 0; i < n; ++i)
             splits[i] = std::max(1, std::min((tiles[i] + best_budget - 1) / best_budget, kMaxSplits));
-        if (best_cost != INT64_MAX) return;
-        // nothing fits the workspace: fall through and shrink
+        if (best_cost == INT64_MAX) {
+            // nothing fits the workspace: shrink below
+        } else {
+            c->plan_n = n;
+            c->plan_force = c->force_splits;
+            c->plan_tiles.assign(tiles, tiles + n);
+            c->plan_splits.assign(splits, splits + n);
+            return;
+        }
     } else {
         for (int i = 0; i < n; ++i) splits[i] = std::max(1, std::min({c->force_splits, tiles[i], kMaxSplits}));
     }
@@ -264,6 +318,10 @@ void plan_splits(const a2t_cache* c, int n, const int* tiles, const int64_t* flo
         if (ws <= c->dev.ws_floats || mx == 1) break;
         for (int i = 0; i < n; ++i) splits[i] = std::max(1, splits[i] / 2);
     }
+    c->plan_n = n;
+    c->plan_force = c->force_splits;
+    c->plan_tiles.assign(tiles, tiles + n);
+    c->plan_splits.assign(splits, splits + n);
 }
 
 // One attention launch (plus merge) over up to kMaxDesc streams.
@@ -285,11 +343,19 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
     }
     plan_splits(c, n, tiles, floats, nsplit);
+    // descriptors in order of falling tiles per split: the dispatcher starts the
+    // longest workgroups first
+    int ord[kMaxDesc];
+    for (int i = 0; i < n; ++i) ord[i] = i;
+    std::stable_sort(ord, ord + n, [&](int a, int b2) {
+        return (tiles[a] + nsplit[a] - 1) / nsplit[a] > (tiles[b2] + nsplit[b2] - 1) / nsplit[b2];
+    });
     int splits = 1;
     int64_t off = 0;
-    for (int i = 0; i < n; ++i) {
+    for (int k = 0; k < n; ++k) {
+        const int i = ord[k];
         const StreamState& s = c->ss[ids[i]];
-        AttnDesc& d = b.d[i];
+        AttnDesc& d = b.d[k];
         d.s = ids[i];
         d.kept = s.kept;
         d.head = s.head;
