@@ -254,6 +254,12 @@ int a2t_sync(a2t_cache* c);
  * last report, and resets those counters. */
 int a2t_profile_enable(a2t_cache* c, const char* kernel_filter);
 int a2t_kernel_time(a2t_cache* c, const char* kernel, int64_t* launches, double* total_ms);
+/* Creates start/stop event pairs ahead of time so that the next n_launches
+ * timed dispatches take them from a pool instead of creating events (or
+ * collecting finished ones) while the work is being issued.  The pool is
+ * freed with the cache.  Errors: INVALID (n_launches < 0), NODEV, OOM (event
+ * creation failed; the pairs created so far stay in the pool). */
+int a2t_profile_reserve(a2t_cache* c, int32_t n_launches);
 
 /* Static strings. */
 const char* a2t_status_str(int status);
@@ -319,6 +325,9 @@ int a2t_distill_loss(a2t_distill* d, int32_t n_rows, const void* student, int64_
  * timed launches and their summed duration in milliseconds since the last
  * report.  Errors: INVALID, HIP. */
 int a2t_distill_profile_enable(a2t_distill* d, int32_t enable);
+/* Creates event pairs for the next n_launches timed calls ahead of time (as
+ * a2t_profile_reserve).  Errors: INVALID, OOM. */
+int a2t_distill_profile_reserve(a2t_distill* d, int32_t n_launches);
 int a2t_distill_kernel_time(a2t_distill* d, int64_t* launches, double* total_ms);
 
 #ifdef __cplusplus

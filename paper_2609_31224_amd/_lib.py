@@ -37,9 +37,9 @@ EXPORTED = (
     "a2t_cache_create", "a2t_cache_destroy", "a2t_set_stream", "a2t_append",
     "a2t_chunk_attn", "a2t_append_attn", "a2t_decode_attn", "a2t_evict", "a2t_stream_info_get",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
-    "a2t_profile_enable", "a2t_kernel_time", "a2t_status_str", "a2t_abi_version",
-    "a2t_distill_create", "a2t_distill_destroy", "a2t_distill_loss",
-    "a2t_distill_profile_enable", "a2t_distill_kernel_time",
+    "a2t_profile_enable", "a2t_kernel_time", "a2t_profile_reserve", "a2t_status_str",
+    "a2t_abi_version", "a2t_distill_create", "a2t_distill_destroy", "a2t_distill_loss",
+    "a2t_distill_profile_enable", "a2t_distill_profile_reserve", "a2t_distill_kernel_time",
 )
 A2T_ROW_NONE, A2T_ROW_ASR, A2T_ROW_NATIVE = 0, 1, 2
 
@@ -93,6 +93,7 @@ def _load():
         "a2t_sync": (C.c_int, [VP]),
         "a2t_profile_enable": (C.c_int, [VP, C.c_char_p]),
         "a2t_kernel_time": (C.c_int, [VP, C.c_char_p, P(C.c_int64), P(C.c_double)]),
+        "a2t_profile_reserve": (C.c_int, [VP, I32]),
         "a2t_status_str": (C.c_char_p, [C.c_int]),
         "a2t_abi_version": (C.c_int, []),
         "a2t_distill_create": (C.c_int, [I32, I32, I32, I32, I32, VP, P(VP)]),
@@ -100,6 +101,7 @@ def _load():
         "a2t_distill_loss": (C.c_int, [VP, I32, VP, C.c_int64, VP, C.c_int64, P(C.c_int8), P(I32),
                                        P(C.c_int8), P(C.c_int8), C.c_float, VP, VP]),
         "a2t_distill_profile_enable": (C.c_int, [VP, I32]),
+        "a2t_distill_profile_reserve": (C.c_int, [VP, I32]),
         "a2t_distill_kernel_time": (C.c_int, [VP, P(C.c_int64), P(C.c_double)]),
     }
     for name, (res, args) in sig.items():
@@ -318,6 +320,10 @@ def a2t_kernel_time(c: Cache, kernel: str) -> Tuple[int, float]:
     ms = C.c_double()
     _check(_lib.a2t_kernel_time(c.ptr, kernel.encode(), C.byref(n), C.byref(ms)), "a2t_kernel_time")
     return n.value, ms.value
+
+
+def a2t_profile_reserve(c: Cache, n_launches: int) -> None:
+    _check(_lib.a2t_profile_reserve(c.ptr, n_launches), "a2t_profile_reserve")
 
 
 def raw_lib():

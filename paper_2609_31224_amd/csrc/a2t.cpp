@@ -163,7 +163,10 @@ struct ProfScope {
     ProfScope(a2t_cache* cc, const char* name) : c(cc) {
         if (!c->prof_on) return;
         if (!c->prof_filter.empty() && std::strstr(name, c->prof_filter.c_str()) == nullptr) return;
-        prof_harvest(c, false);
+        // recycle finished pairs only when the pool is empty (a2t_profile_reserve
+        // fills it beforehand, so a timed launch costs the host no more than a
+        // plain one)
+        if (c->prof_free.size() < 2) prof_harvest(c, false);
         if (c->prof_free.size() < 2) {
             hipEvent_t a, b;
             if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
@@ -1002,6 +1005,21 @@ int a2t_profile_enable(a2t_cache* c, const char* kernel_filter) {
     if (c->host_only) return A2T_ERR_NODEV;
     c->prof_on = kernel_filter != nullptr;
     c->prof_filter = kernel_filter ? kernel_filter : "";
+    return A2T_OK;
+}
+
+int a2t_profile_reserve(a2t_cache* c, int32_t n_launches) {
+    if (!c || n_launches < 0) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    DeviceGuard dg(c->cfg.device);
+    while ((int64_t)c->prof_free.size() < 2 * (int64_t)n_launches) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) {
+            (void)hipGetLastError();
+            return A2T_ERR_OOM;
+        }
+        c->prof_free.push_back(e);
+    }
     return A2T_OK;
 }
 

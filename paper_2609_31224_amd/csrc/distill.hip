@@ -489,6 +489,21 @@ extern "C" int a2t_distill_profile_enable(a2t_distill* d, int32_t enable) {
     return A2T_OK;
 }
 
+extern "C" int a2t_distill_profile_reserve(a2t_distill* d, int32_t n_launches) {
+    if (!d || n_launches < 0) return A2T_ERR_INVALID;
+    DevGuard g(d->device);
+    while ((int64_t)d->prof_free.size() < (int64_t)n_launches) {
+        hipEvent_t a = nullptr, b = nullptr;
+        if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+            if (a) (void)hipEventDestroy(a);
+            (void)hipGetLastError();
+            return A2T_ERR_OOM;
+        }
+        d->prof_free.push_back({a, b});
+    }
+    return A2T_OK;
+}
+
 extern "C" int a2t_distill_kernel_time(a2t_distill* d, int64_t* launches, double* total_ms) {
     if (!d || !launches || !total_ms) return A2T_ERR_INVALID;
     DevGuard g(d->device);
