@@ -195,6 +195,37 @@ def test_forced_key_splits(gpu, splits):
             os.environ["A2T_SPLITS"] = old
 
 
+@pytest.mark.parametrize("splits,nq", [("3", 1), ("22", 1), ("64", 1), ("22", 4), ("7", 4), ("22", 5)])
+def test_few_query_rows_with_key_splits(gpu, splits, nq):
+    """Few query rows per step (the last n_q = 1, 4 or 5 rows of every unit:
+    4 to 20 rows per KV head) over a cache split into 3 to 64 key ranges, at
+    the config-1 head shape on one stream of 100 units (~2.2 K rows), against
+    the fp64 oracle; with 22 splits and one query row the output is
+    bit-identical across two runs (fixed-order merge)."""
+    cfg = CONFIGS[1]
+    spec = make_workload(cfg, units=100).streams[0]
+    old = os.environ.get("A2T_SPLITS")
+    os.environ["A2T_SPLITS"] = splits
+    outs = []
+    try:
+        for _ in range(2 if splits == "22" and nq == 1 else 1):
+            ls = Lockstep(cfg, 1, [spec], layers_checked=[1], n_layers=2, budgets=[10 ** 6],
+                          window=cfg.window, tol=BF16_TOL, query_rows=nq, check_kv_every=50,
+                          **_bounds([spec], 10 ** 6))
+            try:
+                ls.run()
+            finally:
+                ls.close()
+            outs.append(np.concatenate([x.ravel() for x in ls.outputs]))
+    finally:
+        if old is None:
+            os.environ.pop("A2T_SPLITS", None)
+        else:
+            os.environ["A2T_SPLITS"] = old
+    if len(outs) == 2:
+        assert np.array_equal(outs[0], outs[1])
+
+
 def test_runs_are_bit_identical(gpu):
     cfg = CONFIGS[1]
     spec = make_workload(cfg, units=60).streams[0]
