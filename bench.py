@@ -28,6 +28,12 @@ sessions batched in one cache: for budgets unbounded, 8000, 6000, 4000 and 0
 the full hot path over 600 units; End and Peak resident rows per budget and the
 step time (rate = stream unit-steps/s at budget 4000).
 
+--workload hour: 16 hour-long sessions (3,600 units, budget 8192, window 60)
+and the same sessions with no eviction (the control): the units before the
+timed window are filled by all-layers appends, then the full path is timed
+for each group; peak resident rows and KV bytes per stream for both
+(rate = stream unit-steps/s of the evicting group).
+
 --workload distill: the adaptation objective (Sec. 3.2) on a batch of 16
 short utterances x 12 units (~1,340 prediction rows) over a vocabulary of
 151,936 teacher tokens + 2 added tokens, bf16 logits: losses and the gradient
@@ -79,6 +85,8 @@ METRICS = {
                 "per transcript token, all layers, eviction per unit)", "unit-steps/s"),
     "sweep": ("stream unit-steps/s at budget 4000, 15 ten-minute sessions batched (budget sweep "
               "unbounded/8K/6K/4K/0 reported alongside)", "unit-steps/s"),
+    "hour": ("stream unit-steps/s (append+attn+evict), 16 hour-long sessions with eviction "
+             "(no-eviction control reported alongside)", "unit-steps/s"),
     "distill": ("objective evaluations/s (masked CE + T^2 KL + group-balanced means and the "
                 "student-logit gradient over a 16-utterance batch)", "evaluations/s"),
     "copy": ("device copy bandwidth (read + write bytes per second)", "GB/s"),
@@ -90,6 +98,7 @@ DEFAULTS = {  # warmup, steps, profile steps
     "cadence": (200, 100, 30),
     "sweep": (0, 600, 0),
     "distill": (5, 40, 20),
+    "hour": (0, 100, 20),
     "copy": (3, 20, 0),
 }
 
@@ -371,6 +380,19 @@ def run_stream(args):
         tot_bytes += step_bytes(R_attn, n, moved_total - moved_prev, R_attn, cfg)
         moved_prev = moved_total
     step_gbps = tot_bytes / (total_ms * 1e-3) / 1e9
+    if args.jsonl:
+        # one record per timed unit: residency, rows appended / evicted / moved into the
+        # kept region, algorithmic bytes and the unit's GPU time
+        with open(args.jsonl, "w") as f:
+            moved_prev = clean["moved_before"]
+            for j, (R_attn, n, n_ev, moved_total) in enumerate(R_log):
+                moved = moved_total - moved_prev
+                moved_prev = moved_total
+                f.write(json.dumps({"unit": args.warmup + j, "resident_pre": R_attn, "appended": n,
+                                    "evicted": n_ev, "resident_post": R_attn - n_ev,
+                                    "moved": moved,
+                                    "alg_bytes": step_bytes(R_attn, n, moved, R_attn, cfg),
+                                    "ms": float(clean["step_ms"][j])}) + "\n")
     timed_attn_bytes = float(np.mean([attn_bytes(R, n, cfg) for (R, n, _, _) in timed["R_log"]]))
     peak = clean["peak"]
     rows_no_evict = spec.total_rows()
@@ -714,6 +736,118 @@ def run_cadence(args):
     return two_pass(_cadence_session, args, "attn_tile")
 
 
+# ------------------------------------------------------------------- hour-long sessions
+def run_hour(args):
+    """16 hour-long sessions (3,600 units, budget 8192, window 60), then the same
+    sessions with no eviction (the control).  Each group: the units before the
+    timed window are filled with one all-layers append per unit (plus the
+    eviction check for the evicting group), then --steps units run the full path
+    (a2t_append_attn on every layer, a2t_evict) timed with HIP events, then
+    --profile-steps more units with the attention dispatches timestamped."""
+    cfg = CONFIGS[4]
+    specs = make_workload(cfg, seed=args.seed).streams
+    S, L, Hq, Hkv, D = len(specs), cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    T = min(len(s.steps) for s in specs)
+    steps = min(args.steps, T - 1)
+    prof = min(args.profile_steps, T - steps - 1)
+    t0 = T - steps - prof
+    max_n = cfg.max_unit_rows
+    elt_row = 2 * Hkv * D * 2 * L   # K and V bytes of one cached row over all layers
+    ids = (C.c_int32 * S)(*range(S))
+    budget = (C.c_int32 * S)(*[cfg.budget] * S)
+    metas = []
+    for t in range(T):
+        seg = np.concatenate([s.steps[t].seg for s in specs])
+        pos = np.concatenate([s.steps[t].pos for s in specs])
+        metas.append(((C.c_int32 * S)(*[s.steps[t].n for s in specs]),
+                      (C.c_uint8 * len(seg))(*seg.tolist()), (C.c_int32 * len(pos))(*pos.tolist()),
+                      (C.c_int32 * S)(*[s.steps[t].unit for s in specs]), int(len(seg))))
+    max_tot = max(m[4] for m in metas)
+
+    def group(evict):
+        if evict:
+            unit_rows = max(cfg.budget, cfg.window * max_n) + 2 * max_n
+            kept = max(sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in s.steps)
+                       for s in specs) + 64
+        else:
+            unit_rows, kept = max(s.total_rows() for s in specs) + 64, 64
+        r = Runner(cfg, S, unit_rows, kept, max_n)
+        torch, lib, h = r.torch, r.lib, r.h
+        n_ev, unmet = (C.c_int32 * S)(), (C.c_uint8 * S)()
+        # fill: the all-layers input is packed [L][rows of the unit][Hkv][D]; a view of
+        # the front of one flat buffer has that shape for any row count
+        kflat = r.pool((L * max_tot * Hkv * D,), args.seed + 10)
+        vflat = r.pool((L * max_tot * Hkv * D,), args.seed + 11)
+        for t in range(t0):
+            nrows, seg, pos, unit, tot = metas[t]
+            n_el = L * tot * Hkv * D
+            r.check(lib.a2t_append(h, -1, S, ids, nrows, kflat[:n_el].data_ptr(),
+                                   vflat[:n_el].data_ptr(), seg, pos, unit), "a2t_append")
+            if evict:
+                r.check(lib.a2t_evict(h, S, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
+        torch.cuda.synchronize()
+        P = 2
+        qp = r.pool((P, L, max_tot, Hq, D), args.seed)
+        kp = r.pool((P, L, max_tot, Hkv, D), args.seed + 1)
+        vp = r.pool((P, L, max_tot, Hkv, D), args.seed + 2)
+        out = torch.empty(max_tot, Hq, D, dtype=torch.bfloat16, device=r.dev)
+        sq, skv = max_tot * Hq * D * 2, max_tot * Hkv * D * 2
+        R_log = []
+
+        def run_unit(t, record=False):
+            nrows, seg, pos, unit, _ = metas[t]
+            p = t % P
+            for layer in range(L):
+                oq, okv = (p * L + layer) * sq, (p * L + layer) * skv
+                meta = (seg, pos, unit) if layer == 0 else (None, None, None)
+                r.check(lib.a2t_append_attn(h, layer, S, ids, nrows, kp.data_ptr() + okv,
+                                            vp.data_ptr() + okv, *meta, nrows,
+                                            qp.data_ptr() + oq, out.data_ptr()), "a2t_append_attn")
+            if record:
+                R_log.append(sum(attn_bytes(r.stream_info(i).resident, nrows[i], cfg)
+                                 for i in range(S)))
+            if evict:
+                r.check(lib.a2t_evict(h, S, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
+
+        step_ms, total_ms, t_wall, t_enq = r.timed(lambda j: run_unit(t0 + j), steps)
+        r.timed(lambda j: run_unit(t0 + steps + j, record=True), prof, kernel="attn_tile",
+                launches=prof * L)
+        kern_timed = r.kern_timed
+        peak = max(r.stream_info(i).peak for i in range(S))
+        resident = [r.stream_info(i).resident for i in range(S)]
+        r.close()
+        return {"stream_unit_steps_per_s": S * steps / (total_ms * 1e-3),
+                "ms_per_step": total_ms / steps,
+                "unit_ms": {"mean": float(step_ms.mean()), "p99": float(np.percentile(step_ms, 99)),
+                            "over_1s": int((step_ms > 1000).sum())},
+                "peak_rows_per_stream": peak, "peak_kv_bytes_per_stream": peak * elt_row,
+                "resident_rows_mean_at_end": float(np.mean(resident)),
+                "roofline": roofline("attn_tile", kern_timed,
+                                     float(np.mean(R_log)) if R_log else 0.0, "hour")}
+
+    ev = group(True)
+    ctl = group(False)
+    return {
+        "value": ev["stream_unit_steps_per_s"],
+        "ms_per_step": ev["ms_per_step"],
+        "config": {
+            "workload": "hour-long sessions: 16 streams x 3600 units, budget 8192 rows, recent "
+                        "window 60 units, and the same 16 streams with no eviction (control); "
+                        "36 layers, 32 query / 8 KV heads, head dim 128, bf16",
+            "timed_units": [t0, t0 + steps],
+            "attention_timed_units": [t0 + steps, t0 + steps + prof],
+            "calls": "units before the timed window: one all-layers a2t_append (+ a2t_evict); "
+                     "timed: a2t_append_attn per layer over the 16 streams, a2t_evict",
+            "seed": args.seed,
+        },
+        "roofline": ev["roofline"],
+        "evict": ev,
+        "control": ctl,
+        "peak_reduction": 1.0 - ev["peak_rows_per_stream"] / ctl["peak_rows_per_stream"],
+        "cpu_baseline": None,
+    }
+
+
 # ------------------------------------------------------------------- budget sweep
 def run_sweep(args):
     from synth.streams import make_sessions
@@ -938,6 +1072,8 @@ def main():
                     help="extra steps with every dispatch timestamped (roofline)")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--jsonl", default=None,
+                    help="ten-minute stream: write one JSON record per timed unit to this file")
     ap.add_argument("--cpu-sample-units", type=int, default=64)
     ap.add_argument("--cpu-sample-layers", type=int, default=8)
     ap.add_argument("--unfused", action="store_true",
@@ -955,11 +1091,11 @@ def main():
     args.profile_steps = p if args.profile_steps is None else args.profile_steps
     if args.seed is None:
         args.seed = {"stream": 1, "varlen": 2, "decode": 3, "cadence": 1, "sweep": 1,
-                     "distill": 14, "copy": 0}[args.workload]
+                     "distill": 14, "hour": 4, "copy": 0}[args.workload]
 
     res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode,
            "cadence": run_cadence, "sweep": run_sweep, "distill": run_distill,
-           "copy": run_copy}[args.workload](args)
+           "hour": run_hour, "copy": run_copy}[args.workload](args)
     metric, unit = METRICS[args.workload]
     result = {
         "metric": metric,
