@@ -161,6 +161,24 @@ def test_edge_streams(gpu, dtype, tol, budget, window):
     _report(ls, f"edge {dtype} B{budget} W{window}")
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_edge_streams_config1_heads(gpu, fused):
+    """The edge units at the config-1 head shape (32/8 heads, head dim 128, bf16):
+    the 84-row unit (64 transcript tokens) gives 336 query rows per KV head, three
+    passes of the MFMA kernel over the keys; empty segments, decode rows, a unit
+    with nothing evictable, a prefix; budget 40, window 1, a wrapping ring."""
+    cfg = CONFIGS[1]
+    spec = tiny_stream(EDGE_UNITS, prefix=5, pos_gap=3)
+    ls = Lockstep(cfg, 12, [spec], layers_checked=[0], n_layers=1, budgets=[40], window=1,
+                  tol=BF16_TOL, unit_rows=240, kept_rows=400, max_step=84, fused=fused)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    _report(ls, f"edge cfg1 heads fused={fused}")
+    assert ls.evictions > 5
+
+
 def test_short_cache_single_partial_tile(gpu):
     # R < 64 keys: one partial tile, masked tail
     cfg = CONFIGS[0]
