@@ -225,12 +225,12 @@ bool is_evictable(uint8_t seg) { return seg == A2T_SEG_ACOUSTIC || seg == A2T_SE
 // workgroup to the first CU that frees up, so a launch takes about the makespan
 // of its workgroups dispatched in order over `slots` (= CU count) CUs.  For each
 // tile budget per workgroup (>= 2 tiles) every stream gets the fewest splits that
-// respect it; a workgroup costs its tiles plus a fixed part (first-load latency,
-// partial write: ~2 tiles).  Streams are dispatched longest workgroups first
+// respect it; a workgroup costs its tiles plus a fixed part (setup, first-load
+// latency, partial write: ~5 us, measured, ~4 tiles).  Streams are dispatched longest workgroups first
 // (attn_launch orders the descriptors that way), and the budget with the
 // shortest simulated makespan wins (ties: fewer workgroups, i.e. fewer split
 // partials).  The partials must fit the workspace.
-constexpr int kWgFixedTiles = 2;
+constexpr int kWgFixedTiles = 4;
 
 int64_t launch_makespan(int n, const int* tiles, const int* splits, int Hkv, int slots,
                         std::vector<int>& order, std::vector<int64_t>& heap) {
