@@ -16,8 +16,10 @@ namespace a2t {
 constexpr int kMaxDesc = 64;
 // Keys per attention tile (rows staged per LDS tile).
 constexpr int kTileKeys = 64;
-// Most key splits of one attention launch (the merge stages them in LDS).
+// Most key splits of one attention launch.
 constexpr int kMaxSplits = 128;
+// Query rows per workgroup of the split merge.
+constexpr int kMergeRows = 2;
 
 // Device-side buffers of a cache and its shape.
 struct DevState {

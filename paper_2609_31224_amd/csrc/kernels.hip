@@ -788,35 +788,49 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 }
 
 // ----------------------------------------------------------------- attn_merge
-// grid (row blocks, kv head, stream); each thread owns 4 output elements of
-// one query row.  The splits are read 32 at a time (all loads of a batch in
-// flight together) and combined in fixed split order, so the result is
-// deterministic.
+// grid (row pairs, kv head, stream).  A workgroup combines the key-split
+// partials of two query rows: each thread owns 4 output elements of one row
+// and the splits s = sg, sg + NSG, ... of its split group sg (NSG = 4 at head
+// dim 128), read 8 at a time with all loads of a batch in flight together.
+// The split groups' running (max, sum, O) then combine in LDS in group order.
+// Every row's splits are thus spread over NSG threads and the partials over
+// four times as many workgroups as rows of 4 x 32 threads would give, which is
+// what sets the launch's time: the partials come from memory and a CU streams
+// only so many bytes per microsecond.  The order of every sum is fixed, so the
+// result is deterministic.
 template <typename T, class BT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
-    constexpr int B = 32;
+    constexpr int B = 8;
+    constexpr int MR = kMergeRows;
+    __shared__ float4 s_o[256];
+    __shared__ float2 s_ml[256];
     const AttnDesc d = b.d[blockIdx.z];
     if (d.splits <= 1) return;
     const int G = st.Hq / st.Hkv, M = G * d.n_q, D = st.D, g = blockIdx.y;
-    const int tpr = D / 4;           // threads per query row
-    const int rpb = 256 / tpr;       // query rows per block
-    const int rr = threadIdx.x / tpr, d4 = (threadIdx.x - rr * tpr) * 4;
-    const int mq = blockIdx.x * rpb + rr;
-    if (mq >= M) return;
+    const int tpr = D / 4;          // threads per query row
+    const int tsg = MR * tpr;       // threads per split group
+    const int nsg = 256 / tsg;      // split groups
+    const int sg = threadIdx.x / tsg, r = threadIdx.x - sg * tsg;
+    const int rr = r / tpr, d4 = (r - rr * tpr) * 4;
+    const int mq = blockIdx.x * MR + rr;
+    if (blockIdx.x * MR >= M) return;  // the whole workgroup is past the rows
+    const bool live = mq < M;
+    const int mqc = live ? mq : M - 1;
     const float* po = st.ws + d.ws_off;
     const float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
     const int64_t ostride = (int64_t)st.Hkv * M * D, mstride = (int64_t)st.Hkv * M * 2;
-    const float* orow = po + ((int64_t)g * M + mq) * D + d4;
-    const float* mrow = pml + ((int64_t)g * M + mq) * 2;
+    const float* orow = po + ((int64_t)g * M + mqc) * D + d4;
+    const float* mrow = pml + ((int64_t)g * M + mqc) * 2;
     float mx = -INFINITY, L = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < d.splits; s0 += B) {
+    for (int s0 = sg; s0 < d.splits; s0 += B * nsg) {
         float2 ml[B];
         float4 ov[B];
 #pragma unroll
         for (int j = 0; j < B; ++j) {
-            if (s0 + j < d.splits) {
-                ml[j] = *reinterpret_cast<const float2*>(mrow + (s0 + j) * mstride);
-                ov[j] = *reinterpret_cast<const float4*>(orow + (s0 + j) * ostride);
+            const int s = s0 + j * nsg;
+            if (s < d.splits) {
+                ml[j] = *reinterpret_cast<const float2*>(mrow + s * mstride);
+                ov[j] = *reinterpret_cast<const float4*>(orow + s * ostride);
             } else {
                 ml[j] = make_float2(-INFINITY, 0.f);
                 ov[j] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -841,11 +855,29 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o
         }
         mx = bm;
     }
-    const float inv = 1.f / L;
+    s_o[threadIdx.x] = make_float4(O[0], O[1], O[2], O[3]);
+    s_ml[threadIdx.x] = make_float2(mx, L);
+    __syncthreads();
+    if (sg != 0 || !live) return;
+    float bm = -INFINITY;
+    for (int k = 0; k < nsg; ++k) bm = fmaxf(bm, s_ml[k * tsg + r].x);
+    float Lt = 0.f, Ot[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < nsg; ++k) {
+        const float2 ml = s_ml[k * tsg + r];
+        if (ml.x == -INFINITY) continue;
+        const float w = exp2f(ml.x - bm);
+        const float4 ov = s_o[k * tsg + r];
+        Lt += w * ml.y;
+        Ot[0] += w * ov.x;
+        Ot[1] += w * ov.y;
+        Ot[2] += w * ov.z;
+        Ot[3] += w * ov.w;
+    }
+    const float inv = 1.f / Lt;
     const int i = mq / G, hh = mq - i * G;
     T* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D + d4;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) Elt<T>::store(op + e, O[e] * inv);
+    for (int e = 0; e < 4; ++e) Elt<T>::store(op + e, Ot[e] * inv);
 }
 
 // ---------------------------------------------------------------------- evict
@@ -1051,8 +1083,8 @@ hipError_t launch_attn_valu(const DevState& st, const AttnBatch& b, const void* 
 hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hipStream_t stream,
                              const KTimer& kt) {
     const int G = st.Hq / st.Hkv;
-    const int rpb = 256 / (st.D / 4);
-    const dim3 grid((G * b.max_rows + rpb - 1) / rpb, st.Hkv, b.count);
+    if (st.D / 4 * kMergeRows > 256) return hipErrorInvalidValue;
+    const dim3 grid((G * b.max_rows + kMergeRows - 1) / kMergeRows, st.Hkv, b.count);
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
         if (st.dtype == 0)
