@@ -367,6 +367,9 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         d.q_row0 = q_row0[i];
         d.rope_row0 = s.step_rows - n_q[i];
         d.splits = nsplit[i];
+        const int n_tiles = (d.R + kTileKeys - 1) / kTileKeys;
+        d.tile_q = n_tiles / d.splits;
+        d.tile_r = n_tiles % d.splits;
         splits = std::max(splits, nsplit[i]);
         d.n_new = in_row0 ? s.step_rows : 0;
         d.in_row0 = in_row0 ? in_row0[i] : 0;
@@ -503,6 +506,7 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     d.S = k.n_streams;
     d.Hq = k.n_q_heads;
     d.Hkv = k.n_kv_heads;
+    d.G = k.n_q_heads / k.n_kv_heads;
     d.D = k.head_dim;
     d.dtype = k.dtype;
     d.unit_rows = k.unit_rows;

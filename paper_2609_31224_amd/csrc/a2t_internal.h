@@ -39,6 +39,7 @@ struct DevState {
     float* ws;          // split-K attention partials
     int64_t ws_floats;
     int32_t L, S, Hq, Hkv, D, dtype;
+    int32_t G;          // query heads per KV head (Hq / Hkv)
     int32_t unit_rows, kept_rows, max_step_rows;
     float scale_log2e;  // softmax scale * log2(e)
     double theta;
@@ -93,6 +94,8 @@ struct AttnDesc {
     int32_t splits;    // key splits; 1 = write o directly
     int32_t n_new;     // fused append: the last n_new keys come from the input k/v (else 0)
     int32_t in_row0;   // fused append: first row of this stream in the input k/v
+    int32_t tile_q;    // key tiles per split: split sp takes tile_q tiles, one more if
+    int32_t tile_r;    //   sp < tile_r, starting at tile sp * tile_q + min(sp, tile_r)
     int64_t ws_off;    // float offset of this stream's partials in the workspace
 };
 template <int N>

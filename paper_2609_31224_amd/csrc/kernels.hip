@@ -34,6 +34,7 @@ constexpr uint8_t kSegDelim = 2;
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct bf16_t {
     uint16_t bits;
@@ -407,6 +408,50 @@ __device__ __forceinline__ void lds_wait_all(uint2 (&a)[4], uint2 (&b)[4]) {
                    "+v"(b[3]));
 }
 
+// 16-byte global load issued as inline assembly, so the compiler does not
+// place its own wait (it would wait for every DMA issued after it).  The
+// result is valid only after q_wait() names it.
+template <int OFF>
+__device__ __forceinline__ u32x4 gload16_issue(const void* p) {
+    u32x4 r;
+    asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(r) : "v"(p), "i"(OFF) : "memory");
+    return r;
+}
+// s_waitcnt vmcnt(first three tiles' DMAs) that the listed Q and rotary
+// values depend on: the asm-issued loads before those DMAs are complete
+__device__ __forceinline__ void q_wait(u32x4 (&a)[4], u32x4 (&b)[8]) {
+    asm volatile("s_waitcnt vmcnt(12)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]),
+                   "+v"(b[3]), "+v"(b[4]), "+v"(b[5]), "+v"(b[6]), "+v"(b[7])
+                 :
+                 : "memory");
+}
+__device__ __forceinline__ void q_wait(u32x4 (&a)[2], u32x4 (&b)[4]) {
+    asm volatile("s_waitcnt vmcnt(6)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3])
+                 :
+                 : "memory");
+}
+// qraw[s] = the 16 bytes at qb + 64 s; cs[4 s + e] = the 16 bytes at cb + 256 s + 16 e,
+// issued in the order qraw[0], cs[0..3], qraw[1], cs[4..7], ...
+template <int S, int E>
+struct QLoad {
+    template <int KS, int NC>
+    static __device__ __forceinline__ void run(u32x4 (&qraw)[KS], u32x4 (&cs)[NC], const char* qb,
+                                               const char* cb) {
+        if constexpr (E == 0 && S < KS) qraw[S] = gload16_issue<64 * S>(qb);
+        if constexpr (S < KS / 2) {
+            cs[4 * S + E] = gload16_issue<256 * S + 16 * E>(cb);
+            if constexpr (E < 3)
+                QLoad<S, E + 1>::run(qraw, cs, qb, cb);
+            else
+                QLoad<S + 1, 0>::run(qraw, cs, qb, cb);
+        } else if constexpr (S < KS) {
+            QLoad<S + 1, 0>::run(qraw, cs, qb, cb);
+        }
+    }
+};
+
 template <int D, class BT>
 __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT b,
                                                                  const uint16_t* q, uint16_t* o,
@@ -425,11 +470,20 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 
     const AttnDesc d = b.d[blockIdx.z];
     const int g = blockIdx.y, sp = blockIdx.x;
+    // request every descriptor and shape field the prologue uses at once: a
+    // branch on one field before the others are requested costs one
+    // kernel-argument load latency per level
+    asm volatile("" ::"s"(d.s), "s"(d.kept), "s"(d.head), "s"(d.R), "s"(d.n_q), "s"(d.q_row0),
+                 "s"(d.rope_row0), "s"(d.splits), "s"(d.n_new), "s"(d.in_row0), "s"(d.tile_q),
+                 "s"(d.tile_r));
+    asm volatile("" ::"s"(st.G), "s"(st.Hq), "s"(st.Hkv), "s"(st.S), "s"(st.unit_rows),
+                 "s"(st.kept_rows), "s"(st.max_step_rows), "s"(b.layer), "s"(st.k_kept),
+                 "s"(st.v_kept), "s"(st.k_unit), "s"(st.v_unit), "s"(st.rope));
+    asm volatile("" ::"s"(q), "s"(k_in), "s"(v_in), "s"(st.scale_log2e), "s"(st.ws), "s"(d.ws_off));
     if (sp >= d.splits) return;
-    const int G = st.Hq / st.Hkv, nq = d.n_q, M = G * nq, R = d.R;
+    const int G = st.G, nq = d.n_q, M = G * nq, R = d.R;
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
-    const int n_tiles = (R + kTileKeys - 1) / kTileKeys;
-    const int t0 = sp * n_tiles / d.splits, t1 = (sp + 1) * n_tiles / d.splits;
+    const int t0 = sp * d.tile_q + min(sp, d.tile_r), t1 = t0 + d.tile_q + (sp < d.tile_r ? 1 : 0);
     const int vis0 = R - nq;
     const int kept = d.kept, head = d.head, ring_rows = st.unit_rows;
     const int newbase = R - d.n_new;  // fused append: rows newbase .. R-1 come from k_in / v_in
@@ -583,30 +637,35 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
         const bool active = mw < M;
         const int mq = mw + l16;
 
-        // load order: tile t0 and Q, then tiles t0+1 and t0+2 once Q is rotated
-        // (compiler barriers keep it).  Every workgroup of a launch starts at
-        // once; asking for only one tile first lets the first tiles arrive
-        // early instead of behind all of the launch's bytes, so the first
-        // tile's compute overlaps the transfer of the next two.
-        if (t0 < t1) issue(t0, ring[0]);
-        asm volatile("" ::: "memory");
-        // unconditional loads (rows past M read row M-1 and are zeroed below): a
-        // branch here would merge loaded registers and force an early wait
-        uint4 qraw[KS];
-        float4 cs[KS / 2][4];
+        // load order: Q and its rotary rows, then the first three tiles, all
+        // before any wait (compiler barriers keep the order).  Q heads the
+        // memory queue, so it is rotated while the tiles stream in; every
+        // wave's requests go out in tile order, so tile t0 of every workgroup
+        // tends to arrive first and its compute overlaps the later tiles'
+        // transfer.  Unconditional loads (rows past M read row M-1 and are
+        // zeroed below): a branch here would merge loaded registers and force
+        // an early wait.
+        u32x4 qraw[KS];
+        u32x4 csr[KS / 2 * 4];
         {
             const int mqc = mq < M ? mq : M - 1;
             const int i = mqc / G, hh = mqc - i * G;
             const uint16_t* qp = q + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D;
-            const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)i * (D / 2));
-#pragma unroll
-            for (int s = 0; s < KS; ++s) qraw[s] = *reinterpret_cast<const uint4*>(qp + 32 * s + 8 * lg);
-#pragma unroll
-            for (int s = 0; s < KS / 2; ++s)
-#pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2) cs[s][e2] = cs4[(32 * s + 8 * lg) / 2 + e2];
+            const float2* cp = rope + (int64_t)i * (D / 2);
+            QLoad<0, 0>::run(qraw, csr, reinterpret_cast<const char*>(qp + 8 * lg),
+                             reinterpret_cast<const char*>(cp + 8 * lg));
         }
         asm volatile("" ::: "memory");
+        issue_or_dummy(t0, ring[0]);
+        issue_or_dummy(t0 + 1, ring[1]);
+        issue_or_dummy(t0 + 2, ring[2]);
+        static_assert(OPT == KS, "q_wait counts three tiles of DMAs: 12 at head dim 128, 6 at 64");
+        q_wait(qraw, csr);
+        float4 cs[KS / 2][4];
+#pragma unroll
+        for (int s = 0; s < KS / 2; ++s)
+#pragma unroll
+            for (int e2 = 0; e2 < 4; ++e2) cs[s][e2] = __builtin_bit_cast(float4, csr[4 * s + e2]);
 
         // Q^T operand: rotated, scaled by scale*log2(e), bf16
         bf16x8 qop[KS];
@@ -615,7 +674,7 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
             const float qs = mq < M ? st.scale_log2e : 0.f;
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
-                const uint32_t rw[4] = {qraw[s].x, qraw[s].y, qraw[s].z, qraw[s].w};
+                const uint32_t rw[4] = {qraw[s][0], qraw[s][1], qraw[s][2], qraw[s][3]};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     x[s][2 * e] = __uint_as_float(rw[e] << 16);
@@ -640,10 +699,6 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                                        pack_bf16x2(x[s][4], x[s][5]), pack_bf16x2(x[s][6], x[s][7])));
         }
 
-        // after the rotation, which waited for Q (and so for tile t0)
-        asm volatile("" :: "v"(qop[0]), "v"(qop[KS - 1]) : "memory");
-        issue_or_dummy(t0 + 1, ring[1]);
-        issue_or_dummy(t0 + 2, ring[2]);
         uint32_t vtr_off[DB];
         {
             const int r0 = 4 * lg + (l16 >> 2);  // rows 32c + r0 and +16 share r0's swizzle
@@ -806,7 +861,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o
     __shared__ float2 s_ml[256];
     const AttnDesc d = b.d[blockIdx.z];
     if (d.splits <= 1) return;
-    const int G = st.Hq / st.Hkv, M = G * d.n_q, D = st.D, g = blockIdx.y;
+    const int G = st.G, M = G * d.n_q, D = st.D, g = blockIdx.y;
     const int tpr = D / 4;          // threads per query row
     const int tsg = MR * tpr;       // threads per split group
     const int nsg = 256 / tsg;      // split groups
@@ -1024,6 +1079,10 @@ hipError_t launch_append(const DevState& st, const AppendBatch& b, int n_layers,
         return hipGetLastError();
     });
 }
+
+// the attention kernels take the shape, the descriptor batch and four pointers by value
+static_assert(sizeof(DevState) + sizeof(AttnBatch) + 4 * sizeof(void*) <= 4096,
+              "attention kernel arguments must stay within 4 KiB");
 
 hipError_t launch_attn_tile(const DevState& st, const AttnBatch& b, const void* q, void* o,
                             const void* k_in, const void* v_in, hipStream_t stream,
