@@ -408,6 +408,33 @@ __device__ __forceinline__ void lds_wait_all(uint2 (&a)[4], uint2 (&b)[4]) {
                    "+v"(b[3]));
 }
 
+// 16-byte LDS read issued as inline assembly (the compiler keeps only a few
+// in flight and waits after each pair); valid only after k_wait() names it
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_b128_issue(uint32_t addr) {
+    u32x4 r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+// s_waitcnt lgkmcnt(N) that the listed K operands depend on: LDS reads
+// complete in order, so with N reads issued after them these are complete
+template <int N>
+__device__ __forceinline__ void k_wait(u32x4 (&a)[4], u32x4 (&b)[4]);
+template <>
+__device__ __forceinline__ void k_wait<8>(u32x4 (&a)[4], u32x4 (&b)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(8)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+}
+template <>
+__device__ __forceinline__ void k_wait<4>(u32x4 (&a)[4], u32x4 (&b)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(4)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+}
+template <>
+__device__ __forceinline__ void k_wait<0>(u32x4 (&a)[4], u32x4 (&b)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+}
 // 16-byte global load issued as inline assembly, so the compiler does not
 // place its own wait (it would wait for every DMA issued after it).  The
 // result is valid only after q_wait() names it.
@@ -699,6 +726,9 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                                        pack_bf16x2(x[s][4], x[s][5]), pack_bf16x2(x[s][6], x[s][7])));
         }
 
+        uint32_t koff[KS];  // byte offset of this lane's K operand of k-step s, key block 0
+#pragma unroll
+        for (int s = 0; s < KS; ++s) koff[s] = (uint32_t)(l16 * D + ((4 * s + lg) ^ (l16 & (CPR - 1))) * 8) * 2u;
         uint32_t vtr_off[DB];
         {
             const int r0 = 4 * lg + (l16 >> 2);  // rows 32c + r0 and +16 share r0's swizzle
@@ -719,14 +749,30 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
             f32x4 sacc[4];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) sacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            // every K operand of the tile requested before the first product:
+            // rows kb*16 + l16 share the swizzle of row l16, so key block kb is
+            // an immediate offset from the k-step's address
+            const uint32_t kbuf = lds_addr(&buf.k[0]);
+            u32x4 kop[KS][4];
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
+                kop[s][0] = lds_b128_issue<0>(kbuf + koff[s]);
+                kop[s][1] = lds_b128_issue<16 * D * 2>(kbuf + koff[s]);
+                kop[s][2] = lds_b128_issue<32 * D * 2>(kbuf + koff[s]);
+                kop[s][3] = lds_b128_issue<48 * D * 2>(kbuf + koff[s]);
+            }
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    const int r = kb * 16 + l16, c = 4 * s + lg;
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(&buf.k[r * D + (c ^ (r & (CPR - 1))) * 8]);
-                    sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qop[s], sacc[kb], 0, 0, 0);
-                }
+            for (int h = 0; h < KS; h += 2) {
+                if (h == 0)
+                    k_wait<4 * (KS - 2)>(kop[0], kop[1]);
+                else
+                    k_wait<0>(kop[KS - 2], kop[KS - 1]);
+#pragma unroll
+                for (int s = h; s < h + 2; ++s)
+#pragma unroll
+                    for (int kb = 0; kb < 4; ++kb)
+                        sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[s][kb]),
+                                                                           qop[s], sacc[kb], 0, 0, 0);
             }
             if (kbase + kTileKeys - 1 > vis0) {
 #pragma unroll
