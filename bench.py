@@ -378,6 +378,7 @@ def run_stream(args):
         if kernel is None:
             p0 = args.warmup + args.steps
             res["kern"] = r.profiled(lambda j: run_unit(p0 + j), args.profile_steps)
+            res["kern_steps"] = [p0, p0 + args.profile_steps]
             res["peak"] = r.stream_info(0).peak
         r.close()
         return res
@@ -436,6 +437,7 @@ def run_stream(args):
         **timing_fields(clean["step_ms"], total_ms, args.steps, clean["t_wall"], clean["t_enq"]),
         "timed_pass_ms_per_step": timed["total_ms"] / args.steps,
         "kernels_us": clean["kern"],
+        "kernels_us_steps": clean["kern_steps"],
         "peak_rows": peak,
         "rows_without_eviction": rows_no_evict,
         "peak_reduction": 1.0 - peak / rows_no_evict,
@@ -517,6 +519,7 @@ def _varlen_session(args, kernel):
     kern_timed = r.kern_timed
     p0 = warm + timed_steps
     kern = r.profiled(lambda j: run_step(p0 + j), prof_steps)
+    kern_steps = [p0, p0 + prof_steps]
     unmet_streams = sum(1 for i in range(S) if r.stream_info(i).budget_unmet)
     r.close()
     return {
@@ -535,6 +538,7 @@ def _varlen_session(args, kernel):
         "roofline": roofline("attn_tile", kern_timed, alg, "varlen"),
         **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
         "kernels_us": kern,
+        "kernels_us_steps": kern_steps,
         "streams_budget_unmet_at_end": unmet_streams,
         "cpu_baseline": None,
     }
@@ -625,6 +629,7 @@ def _decode_session(args, kernel):
     kern_timed = r.kern_timed
     p0 = warm + timed_steps
     kern = r.profiled(lambda j: run_step(p0 + j), prof_steps)
+    kern_steps = [p0, p0 + prof_steps]
     mean_R = float(np.mean([r.stream_info(i).resident for i in range(S)]))
     r.close()
     return {
@@ -643,6 +648,7 @@ def _decode_session(args, kernel):
         "roofline": roofline(kname, kern_timed, alg, "decode"),
         **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
         "kernels_us": kern,
+        "kernels_us_steps": kern_steps,
         "cpu_baseline": None,
     }
 
@@ -705,6 +711,7 @@ def _cadence_session(args, kernel):
     kern_timed = r.kern_timed
     p0 = args.warmup + args.steps
     kern = r.profiled(lambda j: run_unit(p0 + j), args.profile_steps)
+    kern_steps = [p0, p0 + args.profile_steps]
     steps_per_unit = sum(len(units[u]) for u in range(args.warmup, p0)) / max(1, args.steps)
     r.close()
     return {
@@ -723,6 +730,7 @@ def _cadence_session(args, kernel):
         "roofline": roofline("attn_tile", kern_timed, alg, "cadence"),
         **timing_fields(step_ms, total_ms, args.steps, t_wall, t_enq),
         "kernels_us": kern,
+        "kernels_us_steps": kern_steps,
         "timed_attention_calls": launches,
         "cpu_baseline": None,
     }
@@ -1084,7 +1092,8 @@ def main():
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--profile-steps", type=int, default=None,
-                    help="extra steps with every dispatch timestamped (roofline)")
+                    help="extra steps after the timed ones with every dispatch timestamped "
+                         "(the per-kernel averages in kernels_us, over kernels_us_steps)")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--jsonl", default=None,
