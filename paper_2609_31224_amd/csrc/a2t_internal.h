@@ -19,7 +19,7 @@ constexpr int kTileKeys = 64;
 // Most key splits of one attention launch.
 constexpr int kMaxSplits = 128;
 // Query rows per workgroup of the split merge.
-constexpr int kMergeRows = 2;
+constexpr int kMergeRows = 4;
 
 // Device-side buffers of a cache and its shape.
 struct DevState {

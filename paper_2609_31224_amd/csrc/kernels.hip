@@ -889,16 +889,15 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 }
 
 // ----------------------------------------------------------------- attn_merge
-// grid (row pairs, kv head, stream).  A workgroup combines the key-split
-// partials of two query rows: each thread owns 4 output elements of one row
-// and the splits s = sg, sg + NSG, ... of its split group sg (NSG = 4 at head
-// dim 128), read 8 at a time with all loads of a batch in flight together.
-// The split groups' running (max, sum, O) then combine in LDS in group order.
-// Every row's splits are thus spread over NSG threads and the partials over
-// four times as many workgroups as rows of 4 x 32 threads would give, which is
-// what sets the launch's time: the partials come from memory and a CU streams
-// only so many bytes per microsecond.  The order of every sum is fixed, so the
-// result is deterministic.
+// grid (row groups, kv head, stream).  A workgroup combines the key-split
+// partials of kMergeRows query rows: each thread owns 4 output elements of one
+// row and the splits s = sg, sg + NSG, ... of its split group sg (NSG = 2 at
+// head dim 128), read 8 at a time with all loads of a batch in flight
+// together.  The split groups' running (max, sum, O) then combine in LDS in
+// group order.  Spreading a row's splits over NSG threads spreads the partials
+// over more workgroups than one thread per four outputs would: the partials
+// come from memory and a CU streams only so many bytes per microsecond.  The
+// order of every sum is fixed, so the result is deterministic.
 template <typename T, class BT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
     constexpr int B = 8;
