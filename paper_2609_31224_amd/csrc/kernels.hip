@@ -892,15 +892,15 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 // grid (row groups, kv head, stream).  A workgroup combines the key-split
 // partials of kMergeRows query rows: each thread owns 4 output elements of one
 // row and the splits s = sg, sg + NSG, ... of its split group sg (NSG = 2 at
-// head dim 128), read 8 at a time with all loads of a batch in flight
-// together.  The split groups' running (max, sum, O) then combine in LDS in
-// group order.  Spreading a row's splits over NSG threads spreads the partials
+// head dim 128), read B at a time with all loads of a batch in flight
+// together (the launch picks B = 12 when more than 16 splits would take two
+// rounds of 8, else 8, which holds fewer registers).  The split groups'
+// running (max, sum, O) then combine in LDS in group order.  Spreading a row's splits over NSG threads spreads the partials
 // over more workgroups than one thread per four outputs would: the partials
 // come from memory and a CU streams only so many bytes per microsecond.  The
 // order of every sum is fixed, so the result is deterministic.
-template <typename T, class BT>
+template <typename T, int B, class BT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
-    constexpr int B = 8;
     constexpr int MR = kMergeRows;
     __shared__ float4 s_o[256];
     __shared__ float2 s_ml[256];
@@ -1189,14 +1189,22 @@ hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hi
     const int G = st.Hq / st.Hkv;
     if (st.D / 4 * kMergeRows > 256) return hipErrorInvalidValue;
     const dim3 grid((G * b.max_rows + kMergeRows - 1) / kMergeRows, st.Hkv, b.count);
+    const int nsg = 256 / (kMergeRows * st.D / 4);                // split groups per workgroup
+    const bool wide = (b.max_splits + nsg - 1) / nsg > 8;          // more than one round of 8
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
-        if (st.dtype == 0)
-            A2T_DISPATCH((attn_merge_kernel<float, B>), grid, dim3(256), stream, kt, st, bb,
-                               static_cast<float*>(o));
+        if (st.dtype == 0 && wide)
+            A2T_DISPATCH((attn_merge_kernel<float, 12, B>), grid, dim3(256), stream, kt, st, bb,
+                         static_cast<float*>(o));
+        else if (st.dtype == 0)
+            A2T_DISPATCH((attn_merge_kernel<float, 8, B>), grid, dim3(256), stream, kt, st, bb,
+                         static_cast<float*>(o));
+        else if (wide)
+            A2T_DISPATCH((attn_merge_kernel<bf16_t, 12, B>), grid, dim3(256), stream, kt, st, bb,
+                         static_cast<bf16_t*>(o));
         else
-            A2T_DISPATCH((attn_merge_kernel<bf16_t, B>), grid, dim3(256), stream, kt, st, bb,
-                               static_cast<bf16_t*>(o));
+            A2T_DISPATCH((attn_merge_kernel<bf16_t, 8, B>), grid, dim3(256), stream, kt, st, bb,
+                         static_cast<bf16_t*>(o));
         return hipGetLastError();
     });
 }
