@@ -496,7 +496,12 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
     __shared__ TileBuf<D> ring[kTileStages];
 
     const AttnDesc d = b.d[blockIdx.z];
-    const int g = blockIdx.y, sp = blockIdx.x;
+    // workgroup (split sp, KV head g) is linear block sp * Hkv + g: the dispatcher
+    // deals consecutive workgroups to the 8 XCDs in turn, so with 8 KV heads all
+    // splits of head g run on one XCD and share its L2, where the head's Q and
+    // rotary rows are fetched once instead of once per XCD (any other head
+    // count gives the same results, only without that sharing)
+    const int g = blockIdx.x % st.Hkv, sp = blockIdx.x / st.Hkv;
     // request every descriptor and shape field the prologue uses at once: a
     // branch on one field before the others are requested costs one
     // kernel-argument load latency per level
@@ -889,7 +894,7 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 }
 
 // ----------------------------------------------------------------- attn_merge
-// grid (row groups, kv head, stream).  A workgroup combines the key-split
+// grid (row groups x kv heads, stream).  A workgroup combines the key-split
 // partials of kMergeRows query rows: each thread owns 4 output elements of one
 // row and the splits s = sg, sg + NSG, ... of its split group sg (NSG = 2 at
 // head dim 128), read B at a time with all loads of a batch in flight
@@ -906,14 +911,16 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o
     __shared__ float2 s_ml[256];
     const AttnDesc d = b.d[blockIdx.z];
     if (d.splits <= 1) return;
-    const int G = st.G, M = G * d.n_q, D = st.D, g = blockIdx.y;
+    // row group rg of KV head g is linear block rg * Hkv + g: the XCD of head g,
+    // like the attention workgroups that wrote its partials
+    const int G = st.G, M = G * d.n_q, D = st.D, g = blockIdx.x % st.Hkv, rg = blockIdx.x / st.Hkv;
     const int tpr = D / 4;          // threads per query row
     const int tsg = MR * tpr;       // threads per split group
     const int nsg = 256 / tsg;      // split groups
     const int sg = threadIdx.x / tsg, r = threadIdx.x - sg * tsg;
     const int rr = r / tpr, d4 = (r - rr * tpr) * 4;
-    const int mq = blockIdx.x * MR + rr;
-    if (blockIdx.x * MR >= M) return;  // the whole workgroup is past the rows
+    const int mq = rg * MR + rr;
+    if (rg * MR >= M) return;  // the whole workgroup is past the rows
     const bool live = mq < M;
     const int mqc = live ? mq : M - 1;
     const float* po = st.ws + d.ws_off;
@@ -1134,7 +1141,7 @@ hipError_t launch_attn_tile(const DevState& st, const AttnBatch& b, const void* 
                             const KTimer& kt) {
     const uint16_t* ki = static_cast<const uint16_t*>(k_in);
     const uint16_t* vi = static_cast<const uint16_t*>(v_in);
-    const dim3 grid(b.max_splits, st.Hkv, b.count);
+    const dim3 grid(b.max_splits * st.Hkv, 1, b.count);
     const uint16_t* qq = static_cast<const uint16_t*>(q);
     uint16_t* oo = static_cast<uint16_t*>(o);
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
@@ -1188,7 +1195,7 @@ hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hi
                              const KTimer& kt) {
     const int G = st.Hq / st.Hkv;
     if (st.D / 4 * kMergeRows > 256) return hipErrorInvalidValue;
-    const dim3 grid((G * b.max_rows + kMergeRows - 1) / kMergeRows, st.Hkv, b.count);
+    const dim3 grid((G * b.max_rows + kMergeRows - 1) / kMergeRows * st.Hkv, 1, b.count);
     const int nsg = 256 / (kMergeRows * st.D / 4);                // split groups per workgroup
     const bool wide = (b.max_splits + nsg - 1) / nsg > 8;          // more than one round of 8
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
