@@ -5,6 +5,7 @@ compaction indices bit-exact every step; compaction moves every surviving
 row's bytes unchanged; attention max abs error <= 1e-4 for fp32 caches and
 <= 2e-2 for bf16 caches (fp32 accumulation).
 """
+import dataclasses
 import os
 
 import numpy as np
@@ -58,6 +59,40 @@ def test_config0_shape_bf16_mfma(gpu, seed):
     finally:
         ls.close()
     _report(ls, f"cfg0-bf16 seed{seed}")
+    assert ls.evictions > 40
+
+
+@pytest.mark.parametrize("hq,hkv,d,splits,fused", [
+    (8, 2, 128, None, False),   # two KV heads, group 4
+    (24, 3, 64, "5", True),     # KV-head count that does not divide the 8 XCDs, group 8
+    (32, 4, 128, "9", False),   # group 8 at head dim 128, forced splits
+    (16, 16, 64, None, True),   # multi-head attention (group 1)
+])
+def test_other_gqa_shapes_bf16(gpu, hq, hkv, d, splits, fused):
+    """The MFMA attention at head shapes other than the workloads': workgroup
+    (split, KV head) numbering for any KV-head count, query groups of 1 to 8
+    heads, head dims 64 and 128, planned and forced key splits, with and
+    without the fused append; config 0's stream structure, bf16, against the
+    fp64 oracle."""
+    cfg = dataclasses.replace(CONFIGS[0], n_q_heads=hq, n_kv_heads=hkv, head_dim=d)
+    spec = make_workload(cfg, seed=11).streams[0]
+    old = os.environ.get("A2T_SPLITS")
+    if splits:
+        os.environ["A2T_SPLITS"] = splits
+    try:
+        ls = Lockstep(cfg, 11, [spec], layers_checked=[0], n_layers=1, budgets=[cfg.budget],
+                      window=cfg.window, tol=BF16_TOL, dtype="bf16", fused=fused,
+                      **_bounds([spec], cfg.budget))
+        try:
+            ls.run()
+        finally:
+            ls.close()
+    finally:
+        if old is None:
+            os.environ.pop("A2T_SPLITS", None)
+        else:
+            os.environ["A2T_SPLITS"] = old
+    _report(ls, f"heads {hq}/{hkv} D{d} splits {splits or 'planned'}{' fused' if fused else ''}")
     assert ls.evictions > 40
 
 
