@@ -426,11 +426,6 @@ __device__ __forceinline__ void k_wait<8>(u32x4 (&a)[4], u32x4 (&b)[4]) {
                  : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
 }
 template <>
-__device__ __forceinline__ void k_wait<4>(u32x4 (&a)[4], u32x4 (&b)[4]) {
-    asm volatile("s_waitcnt lgkmcnt(4)"
-                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
-}
-template <>
 __device__ __forceinline__ void k_wait<0>(u32x4 (&a)[4], u32x4 (&b)[4]) {
     asm volatile("s_waitcnt lgkmcnt(0)"
                  : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
