@@ -5,9 +5,13 @@ one listening unit of one stream through every layer: per layer an append
 (rotary keys into the cache) and causal chunk attention of the unit's rows
 over the resident cache, then budgeted eviction and compaction (36 layers,
 32 query / 8 KV heads, head dim 128, bf16, budget 4096 rows, recent window
-30 units).  The session runs from unit 0; the first --warmup units (the cache
-fills and eviction starts near unit 186) are untimed, the next --steps units
-are timed with HIP events on the cache's stream.
+30 units).  The 600-unit session always starts with 200 untimed units that
+bring the cache to steady state (it first exceeds the budget near unit 186);
+then --warmup more units run untimed and the next --steps units are timed
+with HIP events on the cache's stream (warmup + steps <= 400, so every timed
+unit lies inside the session, at steady state with eviction running); the
+session then runs on untimed to unit 600, whose peak residency gives the
+peak-KV reduction.  The oracle's CPU baseline runs the first timed units.
 
 --workload varlen: 32 streams of 60..600 units with random start steps and
 budgets of 2048 or 4096 rows, all active streams of a global step batched in
@@ -93,7 +97,7 @@ METRICS = {
     "copy": ("device copy bandwidth (read + write bytes per second)", "GB/s"),
 }
 DEFAULTS = {  # warmup, steps, profile steps
-    "stream": (200, 400, 100),
+    "stream": (3, 397, 0),
     "varlen": (100, 400, 100),
     "decode": (20, 150, 30),
     "cadence": (200, 100, 30),
@@ -133,12 +137,14 @@ def _threads_used() -> int:
 
 
 def cpu_baseline(cfg, spec, seed, start_unit, sample_units, sample_layers):
-    """Time the float64 oracle on a bounded sample: resumed at a steady-state
-    unit, ``sample_units`` unit steps over ``sample_layers`` layers, scaled to
-    all layers.  The oracle is test infrastructure; only this leg runs it."""
+    """Time the float64 oracle on a bounded sample: resumed at ``start_unit`` (the
+    first unit the GPU leg times), ``sample_units`` unit steps over the first
+    ``sample_layers`` layers, scaled to all layers.  The oracle is test
+    infrastructure; only this leg runs it."""
     from oracle.replay import resume
+    sample_layers = max(1, min(sample_layers, cfg.n_layers))
     layers = list(range(sample_layers))
-    cache = resume(cfg, seed, spec, cfg.budget, cfg.window, start_unit, layers)
+    cache = resume(cfg, seed, spec, spec.budget, cfg.window, start_unit, layers)
     vals = [step_values(cfg, seed, spec.stream, spec.steps[u].key, spec.steps[u].n, layers)
             for u in range(start_unit, start_unit + sample_units)]
     t0 = time.perf_counter()
@@ -153,10 +159,41 @@ def cpu_baseline(cfg, spec, seed, start_unit, sample_units, sample_layers):
     dt = time.perf_counter() - t0
     per_unit_all_layers = dt / sample_units * (cfg.n_layers / sample_layers)
     return {"value": 1.0 / per_unit_all_layers, "unit": "unit-steps/s", "cores": _threads_used(),
-            "kind": "oracle",
-            "sample": f"{sample_units} steady-state units (from unit {start_unit}) x "
-                      f"{sample_layers} of {cfg.n_layers} layers, fp64 numpy, scaled to "
-                      f"{cfg.n_layers} layers; {dt:.1f} s of CPU work"}
+            "kind": "oracle", "cpu_model": _cpu_model(), "host_cpus": os.cpu_count(),
+            "units": [start_unit, start_unit + sample_units],
+            "sample": f"units {start_unit}..{start_unit + sample_units - 1} (the first timed units "
+                      f"of the GPU leg) x {sample_layers} of {cfg.n_layers} layers, append + "
+                      f"attention + eviction, fp64 numpy, scaled to {cfg.n_layers} layers; "
+                      f"{dt:.1f} s of CPU work"}
+
+
+def cpu_baseline_slice(cfg, seed, picks, n_steps, unit):
+    """Time the float64 oracle on a fixed slice of a batched workload: for each
+    (stream spec, first step) in ``picks`` the oracle is resumed at that step
+    and runs ``n_steps`` steps (append, attention of the step's rows on every
+    layer, the eviction check), all layers.  Only the oracle's calls are
+    timed (not the regeneration of inputs).  Rate = stream steps per second."""
+    from oracle.replay import resume
+    layers = list(range(cfg.n_layers))
+    caches = [resume(cfg, seed, spec, spec.budget, cfg.window, k0, layers) for spec, k0 in picks]
+    dt = 0.0
+    for j in range(n_steps):
+        for (spec, k0), cache in zip(picks, caches):
+            st = spec.steps[k0 + j]
+            v = step_values(cfg, seed, spec.stream, st.key, st.n, layers)
+            t0 = time.perf_counter()
+            cache.append(st.seg, st.pos, st.unit, {l: v["k"][i] for i, l in enumerate(layers)},
+                         {l: v["v"][i] for i, l in enumerate(layers)})
+            for i, l in enumerate(layers):
+                cache.attention(l, v["q"][i], st.n)
+            if st.evict:
+                cache.evict(spec.budget, cfg.window)
+            dt += time.perf_counter() - t0
+    return {"value": len(picks) * n_steps / dt, "unit": unit, "cores": _threads_used(),
+            "kind": "oracle", "cpu_model": _cpu_model(), "host_cpus": os.cpu_count(),
+            "sample": f"{n_steps} steady-state steps x {len(picks)} streams "
+                      f"({', '.join(f'stream {sp.stream} from step {k0}' for sp, k0 in picks)}) "
+                      f"x all {cfg.n_layers} layers, fp64 numpy; {dt:.1f} s of CPU work"}
 
 
 class Runner:
@@ -247,11 +284,12 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_31224_amd", "csrc", "kernels.hip")
 
 
-def measured_traffic(workload, kernel):
+def measured_traffic(workload, kernel, units=None):
     """HBM bytes per launch of ``kernel`` in ``workload`` from the committed
     rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE, scaled by a plain
     copy's readings), or None when the summary was taken on other kernel
-    source than the one built here."""
+    source than the one built here, or (with ``units``) over other steps than
+    the ones timed now."""
     import hashlib
     import re
     try:
@@ -265,10 +303,13 @@ def measured_traffic(workload, kernel):
     rec = json.loads(m.group(1))
     if rec.get("source_sha256") != sha:
         return None
-    return rec.get(workload, {}).get(kernel, {}).get("bytes")
+    entry = rec.get(workload, {}).get(kernel, {})
+    if units is not None and list(entry.get("units", [])) != list(units):
+        return None
+    return entry.get("bytes")
 
 
-def roofline(kernel, kern, alg_bytes, workload):
+def roofline(kernel, kern, alg_bytes, workload, units=None):
     """Roofline of ``kernel`` over the timed steps: algorithmic bytes per launch
     over its mean dispatch duration.  The durations come from a second pass
     over the same steps (fresh cache, same inputs) whose dispatches of the
@@ -276,11 +317,13 @@ def roofline(kernel, kern, alg_bytes, workload):
     issue rate, so the pass that gives the rate runs without them."""
     us = kern.get(kernel, {}).get("avg_us")
     achieved = alg_bytes / (us * 1e-6) / 1e9 if us else None
+    traffic = measured_traffic(workload, kernel, units)
     return {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBPS,
             "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS if achieved else None,
-            "traffic": measured_traffic(workload, kernel), "avg_launch_us": us,
+            "traffic": traffic, "avg_launch_us": us,
             "launches_timed": kern.get(kernel, {}).get("launches"),
             "alg_bytes_per_launch": alg_bytes,
+            "traffic_over_alg": traffic / alg_bytes if traffic else None,
             "timing": "per-dispatch start/stop events on the cache's stream, in a second pass "
                       "over the timed steps"}
 
@@ -293,11 +336,53 @@ def timing_fields(step_ms, total_ms, steps, t_wall, t_enqueue):
 
 
 # ------------------------------------------------------------ ten-minute stream
+SESSION_UNITS = 600   # a ten-minute session of one-second units
+FILL_UNITS = 200      # the cache first exceeds the 4096-row budget near unit 186
+
+# The paper's own figures for this workload (context, not the target: whole-model
+# times on other hardware, which a kernel-only unit step does not compare with).
+PAPER_CONTEXT = {
+    "peak_kv_reduction": {
+        "value": 0.646, "positions_unbounded": 11350, "positions_at_budget": 4020,
+        "budget": "4K", "hardware": "1x H100 80GB, batch 1",
+        "workload": "LongSpeech ten-minute sessions, the adapted model with vs without eviction",
+        "source": "Sec. 4.5, Table 3"},
+    "unit_time_ms_at_4k_budget": {
+        "mean": 461, "p99": 675, "share_over_1s": 0.0, "hardware": "1x H100 80GB, batch 1",
+        "scope": "whole model per one-second unit, side-channel decoding and eviction included",
+        "source": "Table 3"},
+    "listening_slack_ms_per_unit": {
+        "value": 900, "hardware": "the paper's setup (its only stated GPU: 1x H100 80GB)",
+        "source": "Sec. 1"},
+}
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def run_stream(args):
-    base = CONFIGS[1]
-    total_units = args.warmup + args.steps + args.profile_steps
-    cfg = dataclasses.replace(base, units=max(base.units, total_units))
-    spec = make_workload(cfg, seed=args.seed, units=total_units).streams[0]
+    """The ten-minute session (600 units) of one stream.  Units 0 .. FILL_UNITS-1
+    bring the cache to steady state untimed (eviction starts near unit 186), then
+    --warmup more units run untimed and the next --steps units are timed; the
+    session then runs on, untimed, to unit 600, whose peak residency gives the
+    peak-KV reduction.  Every timed unit lies inside the session."""
+    cfg = CONFIGS[1]
+    first = FILL_UNITS + args.warmup
+    if args.warmup < 0 or args.steps < 1 or first + args.steps > SESSION_UNITS:
+        raise SystemExit(f"the timed units [{first}, {first + args.steps}) must lie inside the "
+                         f"{SESSION_UNITS}-unit session after the {FILL_UNITS}-unit fill: "
+                         f"--warmup + --steps <= {SESSION_UNITS - FILL_UNITS}")
+    last = first + args.steps
+    spec = make_workload(cfg, seed=args.seed).streams[0]
+    assert len(spec.steps) == SESSION_UNITS
     L, Hq, Hkv, D = cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     max_n = cfg.max_unit_rows
     keep_rows = sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in spec.steps)
@@ -310,11 +395,12 @@ def run_stream(args):
         metas.append(((C.c_int32 * 1)(n), (C.c_uint8 * n)(*st.seg.tolist()),
                       (C.c_int32 * n)(*st.pos.tolist()), (C.c_int32 * 1)(st.unit)))
 
-    def session(kernel):
-        """The stream from unit 0: warmup, then the timed units; with ``kernel``
-        that kernel's dispatches on every ATTN_SAMPLE-th layer of those units are
-        timestamped (a timestamped dispatch slows the host's issue rate; timing one
-        layer in nine changes the unit time by ~3 %, timing all of them by ~40 %)."""
+    def session(mode):
+        """One pass over the session.  mode None: the rate; "attn": the attention
+        dispatches of every ATTN_SAMPLE-th layer of the timed units carry start/stop
+        events (timing one layer in nine changes the unit time by ~3 %, all of them
+        by ~40 %); "all": every dispatch of the timed units is timestamped (the
+        per-kernel averages)."""
         r = Runner(cfg, 1, unit_rows, keep_rows + 64, max_n)
         torch, lib, h = r.torch, r.lib, r.h
         qp = torch.empty(POOL, L, max_n, Hq, D, dtype=torch.bfloat16, device=r.dev)
@@ -342,9 +428,9 @@ def run_stream(args):
                 off_q = (p * L + layer) * row_stride_q
                 off_kv = (p * L + layer) * row_stride_kv
                 meta = (seg, pos, unit) if layer == 0 else (None, None, None)
-                timed_layer = kernel is not None and record and layer % ATTN_SAMPLE == 0
+                timed_layer = mode == "attn" and record and layer % ATTN_SAMPLE == 0
                 if timed_layer:
-                    r.a2t.a2t_profile_enable(r.cache, kernel)
+                    r.a2t.a2t_profile_enable(r.cache, "attn_tile")
                 if args.unfused:
                     r.check(lib.a2t_append(h, layer, 1, ids, nrows, k_base + off_kv,
                                            v_base + off_kv, *meta), "a2t_append")
@@ -362,36 +448,44 @@ def run_stream(args):
             if record:
                 R_log.append((R_attn, nrows[0], int(n_ev[0]), r.stream_info(0).moved_total))
 
-        for u in range(args.warmup):
+        for u in range(first):
             run_unit(u)
         res = {"moved_before": r.stream_info(0).moved_total}
-        if kernel:
-            r.a2t.a2t_profile_reserve(r.cache, args.steps * ((L + ATTN_SAMPLE - 1) // ATTN_SAMPLE))
-        res["step_ms"], res["total_ms"], res["t_wall"], res["t_enq"] = r.timed(
-            lambda j: run_unit(args.warmup + j, record=True), args.steps)
+        if mode == "all":
+            res["kern"] = r.profiled(lambda j: run_unit(first + j, record=True), args.steps)
+        else:
+            if mode == "attn":
+                r.a2t.a2t_profile_reserve(r.cache,
+                                          args.steps * ((L + ATTN_SAMPLE - 1) // ATTN_SAMPLE))
+            res["step_ms"], res["total_ms"], res["t_wall"], res["t_enq"] = r.timed(
+                lambda j: run_unit(first + j, record=True), args.steps)
         res["R_log"] = list(R_log)
         res["kern_timed"] = {}
-        if kernel:
-            n_launch, ms = r.a2t.a2t_kernel_time(r.cache, kernel)
+        if mode == "attn":
+            n_launch, ms = r.a2t.a2t_kernel_time(r.cache, "attn_tile")
             if n_launch:
-                res["kern_timed"][kernel] = {"launches": n_launch, "avg_us": ms * 1e3 / n_launch}
-        if kernel is None:
-            p0 = args.warmup + args.steps
-            res["kern"] = r.profiled(lambda j: run_unit(p0 + j), args.profile_steps)
-            res["kern_steps"] = [p0, p0 + args.profile_steps]
+                res["kern_timed"]["attn_tile"] = {"launches": n_launch,
+                                                  "avg_us": ms * 1e3 / n_launch}
+        if mode is None:
+            for u in range(last, SESSION_UNITS):
+                run_unit(u)
+            r.torch.cuda.synchronize()
             res["peak"] = r.stream_info(0).peak
+            res["end_rows"] = r.stream_info(0).resident
         r.close()
         return res
 
-    clean = session(None)           # the rate
-    timed = session("attn_tile")    # the same units again, attention dispatches timestamped
+    clean = session(None)     # the rate, then the rest of the session for its peak
+    timed = session("attn")   # the same units again, attention dispatches timestamped
+    prof = session("all")     # and once more with every dispatch timestamped
     R_log = clean["R_log"]
     total_ms = clean["total_ms"]
     ms_per_step = total_ms / args.steps
-    # algorithmic bytes of the timed steps
-    moved_prev, tot_bytes = clean["moved_before"], 0
+    # algorithmic bytes of the timed units
+    moved_prev, tot_bytes, moved_sum = clean["moved_before"], 0, 0
     for (R_attn, n, _, moved_total) in R_log:
         tot_bytes += step_bytes(R_attn, n, moved_total - moved_prev, R_attn, cfg)
+        moved_sum += moved_total - moved_prev
         moved_prev = moved_total
     step_gbps = tot_bytes / (total_ms * 1e-3) / 1e9
     if args.jsonl:
@@ -402,7 +496,7 @@ def run_stream(args):
             for j, (R_attn, n, n_ev, moved_total) in enumerate(R_log):
                 moved = moved_total - moved_prev
                 moved_prev = moved_total
-                f.write(json.dumps({"unit": args.warmup + j, "resident_pre": R_attn, "appended": n,
+                f.write(json.dumps({"unit": first + j, "resident_pre": R_attn, "appended": n,
                                     "evicted": n_ev, "resident_post": R_attn - n_ev,
                                     "moved": moved,
                                     "alg_bytes": step_bytes(R_attn, n, moved, R_attn, cfg),
@@ -410,13 +504,14 @@ def run_stream(args):
     timed_attn_bytes = float(np.mean([attn_bytes(R, n, cfg) for (R, n, _, _) in timed["R_log"]]))
     peak = clean["peak"]
     rows_no_evict = spec.total_rows()
+    resident = [R for (R, _, _, _) in R_log]
+    evicted = [e for (_, _, e, _) in R_log]
 
     base_line = None
     if not args.no_cpu_baseline:
-        start = min(400, max(200, args.warmup))
-        base_spec = make_workload(base, seed=args.seed).streams[0]
-        base_line = cpu_baseline(base, base_spec, args.seed, start, args.cpu_sample_units,
-                                 args.cpu_sample_layers)
+        k = max(1, min(args.steps, args.cpu_sample_units))
+        base_line = cpu_baseline(cfg, spec, args.seed, first, k, args.cpu_sample_layers)
+    traffic_units = [first, last]
     res = {
         "value": 1000.0 / ms_per_step,
         "ms_per_step": ms_per_step,
@@ -424,27 +519,39 @@ def run_stream(args):
             "workload": "ten-minute single stream: 36 layers, 32 query / 8 KV heads, head dim 128, "
                         "bf16, units of 17 acoustic + 2 delimiter + Poisson(3) transcript rows, "
                         "budget 4096 rows, recent window 30 units",
-            "timed_units": [args.warmup, args.warmup + args.steps],
+            "session_units": SESSION_UNITS,
+            "fill_units": FILL_UNITS,
+            "timed_units": [first, last],
             "calls": "a2t_append + a2t_chunk_attn per layer" if args.unfused
                      else "a2t_append_attn per layer",
             "seed": args.seed,
         },
-        "roofline": dict(roofline("attn_tile", timed["kern_timed"], timed_attn_bytes, "stream"),
+        "timed_window": {
+            "units": [first, last],
+            "resident_rows_before_eviction": [int(min(resident)), int(max(resident))],
+            "evicting_units": int(sum(1 for e in evicted if e > 0)),
+            "rows_evicted": int(sum(evicted)),
+            "rows_moved_to_kept": int(moved_sum),
+        },
+        "roofline": dict(roofline("attn_tile", timed["kern_timed"], timed_attn_bytes, "stream",
+                                  traffic_units),
                          timing=f"per-dispatch start/stop events on the cache's stream, in a second "
                                 f"pass over the timed units, on every {ATTN_SAMPLE}th layer"),
         "step_hbm": {"achieved_gbps": step_gbps, "frac": step_gbps / HBM_PEAK_GBPS,
                      "alg_bytes_per_step": tot_bytes / max(1, args.steps)},
         **timing_fields(clean["step_ms"], total_ms, args.steps, clean["t_wall"], clean["t_enq"]),
         "timed_pass_ms_per_step": timed["total_ms"] / args.steps,
-        "kernels_us": clean["kern"],
-        "kernels_us_steps": clean["kern_steps"],
+        "kernels_us": prof["kern"],
+        "kernels_us_steps": [first, last],
         "peak_rows": peak,
+        "end_rows": clean["end_rows"],
         "rows_without_eviction": rows_no_evict,
         "peak_reduction": 1.0 - peak / rows_no_evict,
+        "peak_reduction_units": SESSION_UNITS,
+        "paper_context": PAPER_CONTEXT,
         "cpu_baseline": base_line,
     }
     return res
-
 
 # ------------------------------------------------------------------- varlen batch
 def _varlen_session(args, kernel):
@@ -522,6 +629,14 @@ def _varlen_session(args, kernel):
     kern_steps = [p0, p0 + prof_steps]
     unmet_streams = sum(1 for i in range(S) if r.stream_info(i).budget_unmet)
     r.close()
+    base_line = None
+    if kernel is None and not args.no_cpu_baseline:
+        # 10 steps of 4 streams running at the first timed global step (longest histories)
+        cand = [s for s in specs if 0 <= warm - s.offset and warm - s.offset + 10 <= len(s.steps)]
+        cand.sort(key=lambda s: -(warm - s.offset))
+        picks = [(s, warm - s.offset) for s in cand[:4]]
+        if picks:
+            base_line = cpu_baseline_slice(cfg, args.seed, picks, 10, "unit-steps/s")
     return {
         "value": stream_steps / (total_ms * 1e-3),
         "ms_per_step": total_ms / max(1, timed_steps),
@@ -540,7 +655,7 @@ def _varlen_session(args, kernel):
         "kernels_us": kern,
         "kernels_us_steps": kern_steps,
         "streams_budget_unmet_at_end": unmet_streams,
-        "cpu_baseline": None,
+        "cpu_baseline": base_line,
     }
 
 
@@ -632,6 +747,11 @@ def _decode_session(args, kernel):
     kern_steps = [p0, p0 + prof_steps]
     mean_R = float(np.mean([r.stream_info(i).resident for i in range(S)]))
     r.close()
+    base_line = None
+    if kernel is None and not args.no_cpu_baseline and warm + 10 <= n_dec:
+        # 10 decode steps of 4 streams from the first timed decode step
+        picks = [(specs[i], n_units + warm) for i in range(min(4, S))]
+        base_line = cpu_baseline_slice(cfg, args.seed, picks, 10, "decode-steps/s")
     return {
         "value": S * timed_steps / (total_ms * 1e-3),
         "ms_per_step": total_ms / max(1, timed_steps),
@@ -649,7 +769,7 @@ def _decode_session(args, kernel):
         **timing_fields(step_ms, total_ms, max(1, timed_steps), t_wall, t_enq),
         "kernels_us": kern,
         "kernels_us_steps": kern_steps,
-        "cpu_baseline": None,
+        "cpu_baseline": base_line,
     }
 
 
@@ -1098,8 +1218,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--jsonl", default=None,
                     help="ten-minute stream: write one JSON record per timed unit to this file")
-    ap.add_argument("--cpu-sample-units", type=int, default=64)
-    ap.add_argument("--cpu-sample-layers", type=int, default=8)
+    ap.add_argument("--cpu-sample-units", type=int, default=20,
+                    help="ten-minute stream: oracle units timed, from the first timed unit")
+    ap.add_argument("--cpu-sample-layers", type=int, default=36)
     ap.add_argument("--unfused", action="store_true",
                     help="stream workload: per layer a2t_append then a2t_chunk_attn")
     ap.add_argument("--decode-call", choices=("decode", "fused"), default="decode",

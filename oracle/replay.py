@@ -16,7 +16,7 @@ import numpy as np
 from synth.streams import StreamSpec, WorkloadConfig, step_values
 
 from .cache import OracleCache
-from .policy import plan_eviction
+from .policy import compaction_indices, plan_eviction
 
 
 @dataclass
@@ -25,7 +25,11 @@ class StepTrace:
     n_post: int
     units: List[int]
     budget_unmet: bool
-    moved: int                 # survivors at or after the first evicted slot
+    moved: int                 # survivors at or after the first evicted slot: the rows an
+                               # in-place order-preserving compaction would shift
+    settled: int = 0           # survivors that join the retained prefix at this step (below)
+    evict_mask: Optional[np.ndarray] = None   # bool [n_pre] (with record_masks)
+    new_slot: Optional[np.ndarray] = None     # int32 [n_pre] (with record_masks)
 
 
 @dataclass
@@ -40,45 +44,87 @@ class StreamTrace:
     src_row: Optional[np.ndarray] = None
 
 
+class MetadataReplay:
+    """The eviction policy over a stream's steps, one step at a time.
+
+    Besides the plan of each step it reports ``settled``: once a step has
+    evicted units up to u, every resident row of a unit <= u is non-evictable
+    for good (whole units go oldest first), so those rows form a retained
+    prefix of the cache that no later eviction touches; ``settled`` counts the
+    surviving rows of units <= u that were not already in that prefix (rows
+    retained from the units just evicted, and rows appended since the
+    previous eviction under a unit id it had already reached).  A cache that
+    keeps that prefix in a region of its own copies exactly these rows into
+    it when it compacts.
+    """
+
+    def __init__(self, spec: StreamSpec, budget: int, window: int, record_masks: bool = False):
+        self.spec, self.budget, self.window = spec, budget, window
+        self.record_masks = record_masks
+        self.i = 0
+        self.pos = np.zeros(0, np.int64)
+        self.seg = np.zeros(0, np.uint8)
+        self.unit = np.zeros(0, np.int64)
+        self.src_step = np.zeros(0, np.int64)
+        self.src_row = np.zeros(0, np.int64)
+        self.in_prefix = np.zeros(0, bool)
+        self.cur = -1
+        self.peak = 0
+
+    def step(self) -> StepTrace:
+        st = self.spec.steps[self.i]
+        n = st.n
+        self.pos = np.concatenate([self.pos, st.pos.astype(np.int64)])
+        self.seg = np.concatenate([self.seg, st.seg])
+        self.unit = np.concatenate([self.unit, np.full(n, st.unit, np.int64)])
+        self.src_step = np.concatenate([self.src_step, np.full(n, self.i, np.int64)])
+        self.src_row = np.concatenate([self.src_row, np.arange(n, dtype=np.int64)])
+        self.in_prefix = np.concatenate([self.in_prefix, np.zeros(n, bool)])
+        self.i += 1
+        self.cur = max(self.cur, st.unit)
+        self.peak = max(self.peak, self.pos.shape[0])
+        R = self.pos.shape[0]
+        if not st.evict:
+            # Sec. 3.3 checks the budget after each duplex unit: a step that does
+            # not end its unit (a side-channel chunk or token) is not checked
+            tr = StepTrace(R, R, [], False, 0)
+            if self.record_masks:
+                tr.evict_mask = np.zeros(R, bool)
+                tr.new_slot = np.arange(R, dtype=np.int32)
+            return tr
+        plan = plan_eviction(self.seg, self.unit, self.budget, self.window, self.cur)
+        keep = ~plan.evict_mask
+        moved = int(keep[int(np.argmax(plan.evict_mask)):].sum()) if plan.evict_mask.any() else 0
+        settled = 0
+        if plan.units:
+            joins = keep & (self.unit <= max(plan.units)) & ~self.in_prefix
+            settled = int(joins.sum())
+            self.in_prefix |= joins
+        tr = StepTrace(plan.n_pre, plan.n_post, plan.units, plan.budget_unmet, moved, settled)
+        if self.record_masks:
+            tr.evict_mask = plan.evict_mask
+            tr.new_slot = compaction_indices(plan.evict_mask)
+        self.pos, self.seg, self.unit = self.pos[keep], self.seg[keep], self.unit[keep]
+        self.src_step, self.src_row = self.src_step[keep], self.src_row[keep]
+        self.in_prefix = self.in_prefix[keep]
+        return tr
+
+
 def replay_metadata(spec: StreamSpec, budget: int, window: int,
-                    n_steps: Optional[int] = None, evict: bool = True) -> StreamTrace:
-    """Run the eviction policy over the first ``n_steps`` steps of a stream."""
+                    n_steps: Optional[int] = None, evict: bool = True,
+                    record_masks: bool = False) -> StreamTrace:
+    """Run the eviction policy over the first ``n_steps`` steps of a stream.
+    With ``record_masks`` every step also carries its eviction mask and
+    compaction indices (memory grows with steps x resident rows)."""
     n_steps = len(spec.steps) if n_steps is None else n_steps
     if not evict:
         return _replay_no_eviction(spec, n_steps)
-    pos = np.zeros(0, np.int64)
-    seg = np.zeros(0, np.uint8)
-    unit = np.zeros(0, np.int64)
-    src_step = np.zeros(0, np.int64)
-    src_row = np.zeros(0, np.int64)
-    cur = -1
+    rp = MetadataReplay(spec, budget, window, record_masks=record_masks)
     tr = StreamTrace()
-    for i in range(n_steps):
-        st = spec.steps[i]
-        n = st.n
-        pos = np.concatenate([pos, st.pos.astype(np.int64)])
-        seg = np.concatenate([seg, st.seg])
-        unit = np.concatenate([unit, np.full(n, st.unit, np.int64)])
-        src_step = np.concatenate([src_step, np.full(n, i, np.int64)])
-        src_row = np.concatenate([src_row, np.arange(n, dtype=np.int64)])
-        cur = max(cur, st.unit)
-        tr.peak = max(tr.peak, pos.shape[0])
-        if not evict or not st.evict:
-            # Sec. 3.3 checks the budget after each duplex unit: a step that does
-            # not end its unit (a side-channel chunk or token) is not checked
-            tr.steps.append(StepTrace(pos.shape[0], pos.shape[0], [], False, 0))
-            continue
-        plan = plan_eviction(seg, unit, budget, window, cur)
-        keep = ~plan.evict_mask
-        if plan.evict_mask.any():
-            first = int(np.argmax(plan.evict_mask))
-            moved = int(keep[first:].sum())
-        else:
-            moved = 0
-        tr.steps.append(StepTrace(plan.n_pre, plan.n_post, plan.units, plan.budget_unmet, moved))
-        pos, seg, unit = pos[keep], seg[keep], unit[keep]
-        src_step, src_row = src_step[keep], src_row[keep]
-    tr.pos, tr.seg, tr.unit, tr.src_step, tr.src_row = pos, seg, unit, src_step, src_row
+    for _ in range(n_steps):
+        tr.steps.append(rp.step())
+    tr.peak = rp.peak
+    tr.pos, tr.seg, tr.unit, tr.src_step, tr.src_row = rp.pos, rp.seg, rp.unit, rp.src_step, rp.src_row
     return tr
 
 

@@ -5,7 +5,10 @@ pattern of the benchmark: every active stream of a global step goes into one
 call per layer, then one a2t_evict.  What the oracle can afford is checked:
 
 * every stream, every step: rows evicted and the budget flag, against the
-  oracle's metadata-only policy replay (eviction reads no K/V values);
+  oracle's metadata-only policy replay (eviction reads no K/V values); at
+  every step that evicts, the device's eviction mask and compaction indices
+  (bit-exact) and the rows the library copied into its kept region (against
+  the rows that join the oracle's retained prefix);
 * every stream at the end: the device layout (pos, seg, unit per slot);
 * sampled streams on the checked layers: attention outputs at every
   ``check_every``-th step (or at the global steps in ``check_steps``) and the
@@ -41,7 +44,7 @@ class SampledBatch:
         import torch
         import paper_2609_31224_amd as a2t
         from oracle.cache import OracleCache
-        from oracle.replay import replay_metadata
+        from oracle.replay import MetadataReplay, replay_metadata
         self.torch, self.a2t = torch, a2t
         self.cfg, self.seed, self.specs = cfg, seed, specs
         self.sampled = list(sampled)
@@ -60,6 +63,11 @@ class SampledBatch:
                            theta=cfg.rope_theta, scale=cfg.scale) for i in self.sampled}
         self.traces = [replay_metadata(s, b, window, evict=evict)
                        for s, b in zip(specs, self.budgets)]
+        # step-by-step replays that also give each step's mask and compaction indices
+        self.replays = [MetadataReplay(s, b, window, record_masks=True)
+                        for s, b in zip(specs, self.budgets)] if evict else None
+        self.moved = [0] * len(specs)
+        self.mask_checks = 0
         self.T = max(s.offset + len(s.steps) for s in specs)
         max_rows = max(sum(s.steps[t - s.offset].n for s in specs
                            if 0 <= t - s.offset < len(s.steps)) for t in range(self.T))
@@ -158,6 +166,7 @@ class SampledBatch:
                 if check and layer in self.layers_checked:
                     self._check_attention(t, layer, act, offs, vals, o)
         self.layer_loop_s += time.perf_counter() - t0
+        rtr = {i: self.replays[i].step() for i, _ in act} if self.replays else {}
         act = [(i, st) for i, st in act if st.evict]  # checked after the steps ending a unit
         ids = [i for i, _ in act]
         if not act:
@@ -175,11 +184,33 @@ class SampledBatch:
                                f"unmet {unmet[j]}/{tr.budget_unmet}")
             self.evictions += int(want > 0)
             self.unmet_steps += int(tr.budget_unmet)
+            if self.replays:
+                self._check_eviction(t, i, rtr[i], want)
             if i in self.oracles and self.evict:
                 rec = self.oracles[i].evict(self.budgets[i], self.window)
                 assert rec.n_evicted == want
         if self.rebuild:
             self.oracles = {}
+
+    def _check_eviction(self, t, i, rt, want):
+        """The device's mask and compaction indices of this step's eviction, and
+        the rows moved into the kept region, against the oracle's replay."""
+        a2t = self.a2t
+        if rt.n_pre - rt.n_post != want:
+            raise Mismatch(f"{self.label} step {t} stream {i}: replays disagree")
+        moved = a2t.a2t_stream_info_get(self.cache, i)["moved_total"]
+        if moved - self.moved[i] != rt.settled:
+            raise Mismatch(f"{self.label} step {t} stream {i}: moved {moved - self.moved[i]} rows "
+                           f"into the kept region, oracle {rt.settled}")
+        self.moved[i] = moved
+        if want == 0:
+            return
+        n_pre, mask, slot = a2t.a2t_read_last_evict(self.cache, i)
+        if n_pre != rt.n_pre or not np.array_equal(mask.astype(bool), rt.evict_mask) \
+                or not np.array_equal(slot, rt.new_slot):
+            raise Mismatch(f"{self.label} step {t} stream {i}: eviction mask / compaction "
+                           f"indices differ from the oracle")
+        self.mask_checks += 1
 
     def _check_attention(self, t, layer, act, offs, vals, o):
         og = None

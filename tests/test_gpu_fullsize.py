@@ -1,10 +1,13 @@
 """GPU parity at full workload sizes, in the benchmark's batched call pattern.
 
-The batched varlen listening workload (32 streams, 600-step schedule) and the
-speaking-phase decode workload (64 streams, 600-unit fill, 200 decode steps)
-run whole.  Eviction counts, budget flags, final layouts and peaks are checked
-for every stream against the oracle's policy replay; attention and stored
-K/V on sampled streams and layers against the fp64 oracle (bf16 bar 2e-2).
+The benchmark's ten-minute stream in its exact call pattern, the batched
+varlen listening workload (32 streams, 600-step schedule), the speaking-phase
+decode workload (64 streams, 600-unit fill, 200 decode steps) and the
+hour-long sessions run whole.  Eviction counts, budget flags, every
+eviction's mask and compaction indices (bit-exact), the rows moved into the
+kept region, final layouts and peaks are checked for every stream against the
+oracle's policy replay; attention and stored K/V on sampled streams and
+layers against the fp64 oracle (bf16 bar 2e-2).
 """
 import numpy as np
 import pytest
@@ -26,6 +29,31 @@ def _caps(cfg, specs, extra=0):
     return unit_rows, kept, max_n
 
 
+def test_config1_benchmark_path_600_units(gpu):
+    # the benchmark's own path: one ten-minute stream (the bench's seed) through
+    # a2t_append_attn on every layer with the planner's key splits, the bench's ring
+    # size (max(B, W * max_n) + 2 max_n rows, so the ring wraps), then a2t_evict;
+    # attention on layers 0, 17 and 35 at every unit, every eviction's mask and
+    # compaction indices, and the stored K/V at the end
+    cfg = CONFIGS[1]
+    spec = make_workload(cfg, seed=1).streams[0]
+    max_n = cfg.max_unit_rows
+    unit_rows = max(cfg.budget, cfg.window * max_n) + 2 * max_n
+    kept = int(sum(np.isin(st.seg, KEEP).sum() for st in spec.steps)) + 64
+    run = SampledBatch(cfg, 1, [spec], sampled=[0], layers_checked=[0, 17, 35],
+                       budgets=[cfg.budget], window=cfg.window, unit_rows=unit_rows,
+                       kept_rows=kept, max_step=max_n, tol=BF16_TOL, check_every=1,
+                       listen_call="fused", label="cfg1 bench path")
+    try:
+        run.run()
+    finally:
+        run.close()
+    print(f"[cfg1 bench path] evicting units {run.evictions}, mask checks {run.mask_checks}, "
+          f"attention checks {run.attn_checks}, max err {run.max_err:.3e}", flush=True)
+    assert run.attn_checks == 3 * 600
+    assert run.evictions == run.mask_checks > 400
+
+
 def test_config2_full_varlen_batched(gpu):
     cfg = CONFIGS[2]
     specs = make_workload(cfg).streams
@@ -44,8 +72,10 @@ def test_config2_full_varlen_batched(gpu):
     finally:
         run.close()
     print(f"[cfg2 full] evicting stream-steps {run.evictions}, unmet {run.unmet_steps}, "
-          f"attention checks {run.attn_checks}, max err {run.max_err:.3e}", flush=True)
+          f"mask checks {run.mask_checks}, attention checks {run.attn_checks}, "
+          f"max err {run.max_err:.3e}", flush=True)
     assert run.evictions > 1000 and run.unmet_steps > 0 and run.attn_checks > 200
+    assert run.mask_checks == run.evictions
 
 
 @pytest.mark.parametrize("decode_call", ["decode", "fused"])
@@ -61,8 +91,10 @@ def test_config3_full_decode_batched(gpu, decode_call):
         run.run()
     finally:
         run.close()
-    print(f"[cfg3 full {decode_call}] evicting stream-steps {run.evictions}, attention checks "
-          f"{run.attn_checks}, max err {run.max_err:.3e}", flush=True)
+    print(f"[cfg3 full {decode_call}] evicting stream-steps {run.evictions}, mask checks "
+          f"{run.mask_checks}, attention checks {run.attn_checks}, max err {run.max_err:.3e}",
+          flush=True)
+    assert run.mask_checks == run.evictions
     # attention is checked on the decode steps (the fill appends without attention)
     assert run.attn_checks == 2 * 2 * cfg.decode_steps
     assert run.evictions > 64 * 400
@@ -95,8 +127,9 @@ def test_config4_full_hour_long_with_control(gpu):
         finally:
             run.close()
         print(f"[{label}] evicting stream-steps {run.evictions}, unmet {run.unmet_steps}, "
-              f"attention checks {run.attn_checks}, max err {run.max_err:.3e}, "
-              f"peak rows {peaks[evict]}", flush=True)
+              f"mask checks {run.mask_checks}, attention checks {run.attn_checks}, "
+              f"max err {run.max_err:.3e}, peak rows {peaks[evict]}", flush=True)
+        assert run.mask_checks == (run.evictions if evict else 0)
         assert run.attn_checks == 3
         if evict:
             assert run.unmet_steps > 0 and run.evictions > 16 * 3000

@@ -147,9 +147,11 @@ def _library_trace(spec, budget, window, unit_rows, kept_rows, max_step):
     for st in spec.steps:
         append_all(c, 0, st)
         pre = a2t.a2t_stream_info_get(c, 0)["resident"]
+        moved0 = a2t.a2t_stream_info_get(c, 0)["moved_total"]
         n_ev, unmet = a2t.a2t_evict(c, [0], [budget], window)
         info = a2t.a2t_stream_info_get(c, 0)
-        rows.append((pre, int(n_ev[0]), bool(unmet[0]), info["resident"], info["last_evicted_unit"]))
+        rows.append((pre, int(n_ev[0]), bool(unmet[0]), info["resident"], info["last_evicted_unit"],
+                     info["moved_total"] - moved0))
     peak = a2t.a2t_stream_info_get(c, 0)["peak"]
     a2t.a2t_cache_destroy(c)
     return rows, peak
@@ -160,8 +162,10 @@ def _compare(spec, budget, window):
     rows, peak = _library_trace(spec, budget, window, total + 1, total + 1,
                                 max(st.n for st in spec.steps))
     tr = replay_metadata(spec, budget, window)
-    for (pre, n_ev, unmet, post, last_u), t in zip(rows, tr.steps):
+    for (pre, n_ev, unmet, post, last_u, moved), t in zip(rows, tr.steps):
         assert pre == t.n_pre
+        # rows copied into the kept region = rows joining the oracle's retained prefix
+        assert moved == t.settled
         assert n_ev == t.n_pre - t.n_post
         assert unmet == t.budget_unmet
         assert post == t.n_post
