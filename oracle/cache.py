@@ -26,7 +26,7 @@ from synth.streams import SEG_PREFIX, SEG_RESPONSE
 
 from . import rope
 from .attention import attend
-from .policy import EvictionPlan, compaction_indices, plan_eviction
+from .policy import EvictionPlan, EvictRule, compaction_indices, plan_by_rule
 
 
 class OracleError(ValueError):
@@ -160,11 +160,15 @@ class OracleCache:
                       self.scale, visible=self.h_resident)
 
     # -- 3. evict and compact ----------------------------------------------------
-    def evict(self, budget: int, window: int) -> EvictRecord:
+    def evict(self, budget: int, window: int, rule: Optional[EvictRule] = None) -> EvictRecord:
+        """Sec. 3.3's rule after a unit (or, with ``rule``, one of its variants)."""
         if budget < 0 or window < 0:
             raise OracleError("budget and window are non-negative")
+        rule = rule or EvictRule()
+        if rule.kind == "sink_recent" and budget < rule.n_sink:
+            raise OracleError("the budget must cover the sink rows")
         cur = -1 if self.cur is None else self.cur
-        plan = plan_eviction(self.seg, self.unit, budget, window, cur)
+        plan = plan_by_rule(rule, self.seg, self.unit, budget, window, cur)
         new_slot = compaction_indices(plan.evict_mask)
         keep = ~plan.evict_mask
         if self.keep_history and plan.evict_mask.any():

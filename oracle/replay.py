@@ -16,7 +16,7 @@ import numpy as np
 from synth.streams import StreamSpec, WorkloadConfig, step_values
 
 from .cache import OracleCache
-from .policy import compaction_indices, plan_eviction
+from .policy import EvictRule, compaction_indices, plan_by_rule
 
 
 @dataclass
@@ -55,11 +55,16 @@ class MetadataReplay:
     retained from the units just evicted, and rows appended since the
     previous eviction under a unit id it had already reached).  A cache that
     keeps that prefix in a region of its own copies exactly these rows into
-    it when it compacts.
+    it when it compacts.  Under the row and sink+recent variants of the rule
+    (which can stop inside a unit) the prefix ends at the newest evicted row
+    instead: ``settled`` then counts the survivors older than that row that
+    were not already in it.
     """
 
-    def __init__(self, spec: StreamSpec, budget: int, window: int, record_masks: bool = False):
+    def __init__(self, spec: StreamSpec, budget: int, window: int, record_masks: bool = False,
+                 rule: Optional[EvictRule] = None):
         self.spec, self.budget, self.window = spec, budget, window
+        self.rule = rule or EvictRule()
         self.record_masks = record_masks
         self.i = 0
         self.pos = np.zeros(0, np.int64)
@@ -92,12 +97,18 @@ class MetadataReplay:
                 tr.evict_mask = np.zeros(R, bool)
                 tr.new_slot = np.arange(R, dtype=np.int32)
             return tr
-        plan = plan_eviction(self.seg, self.unit, self.budget, self.window, self.cur)
+        plan = plan_by_rule(self.rule, self.seg, self.unit, self.budget, self.window, self.cur)
         keep = ~plan.evict_mask
         moved = int(keep[int(np.argmax(plan.evict_mask)):].sum()) if plan.evict_mask.any() else 0
         settled = 0
         if plan.units:
-            joins = keep & (self.unit <= max(plan.units)) & ~self.in_prefix
+            if self.rule.kind == "unit":
+                older = self.unit <= max(plan.units)
+            else:
+                # the other rules can stop inside a unit: the retained prefix ends
+                # at the newest evicted row
+                older = np.arange(keep.shape[0]) < int(np.flatnonzero(plan.evict_mask)[-1])
+            joins = keep & older & ~self.in_prefix
             settled = int(joins.sum())
             self.in_prefix |= joins
         tr = StepTrace(plan.n_pre, plan.n_post, plan.units, plan.budget_unmet, moved, settled)
@@ -112,14 +123,15 @@ class MetadataReplay:
 
 def replay_metadata(spec: StreamSpec, budget: int, window: int,
                     n_steps: Optional[int] = None, evict: bool = True,
-                    record_masks: bool = False) -> StreamTrace:
-    """Run the eviction policy over the first ``n_steps`` steps of a stream.
-    With ``record_masks`` every step also carries its eviction mask and
-    compaction indices (memory grows with steps x resident rows)."""
+                    record_masks: bool = False, rule: Optional[EvictRule] = None) -> StreamTrace:
+    """Run the eviction policy (``rule``: Sec. 3.3's by default) over the first
+    ``n_steps`` steps of a stream.  With ``record_masks`` every step also
+    carries its eviction mask and compaction indices (memory grows with steps
+    x resident rows)."""
     n_steps = len(spec.steps) if n_steps is None else n_steps
     if not evict:
         return _replay_no_eviction(spec, n_steps)
-    rp = MetadataReplay(spec, budget, window, record_masks=record_masks)
+    rp = MetadataReplay(spec, budget, window, record_masks=record_masks, rule=rule)
     tr = StreamTrace()
     for _ in range(n_steps):
         tr.steps.append(rp.step())
@@ -152,7 +164,8 @@ def _replay_no_eviction(spec: StreamSpec, n_steps: int) -> StreamTrace:
 
 def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window: int,
            n_steps: int, layers: Sequence[int], evict: bool = True,
-           values: Optional[Callable[[int], Dict[str, np.ndarray]]] = None) -> OracleCache:
+           values: Optional[Callable[[int], Dict[str, np.ndarray]]] = None,
+           rule: Optional[EvictRule] = None) -> OracleCache:
     """Oracle cache holding the state of ``spec`` after its first ``n_steps`` steps.
 
     The surviving rows are re-appended in cache order with their original
@@ -162,7 +175,7 @@ def resume(cfg: WorkloadConfig, seed: int, spec: StreamSpec, budget: int, window
     ``values(step_index)`` may supply a step's generated values (arrays ``k``,
     ``v`` of shape ``[len(layers)][n][Hkv][D]``) instead of regenerating them.
     """
-    tr = replay_metadata(spec, budget, window, n_steps, evict=evict)
+    tr = replay_metadata(spec, budget, window, n_steps, evict=evict, rule=rule)
     cache = OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, layers,
                         theta=cfg.rope_theta, scale=cfg.scale)
     # regenerate each surviving row's values from its source step
