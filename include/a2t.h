@@ -32,9 +32,13 @@
  *     returns.  Device buffers must stay valid until the HIP stream reaches
  *     the enqueued work; outputs are ready after the stream does.
  *   - All compute is enqueued on the cache's HIP stream (a2t_set_stream).
- *     Nothing in a2t_append / a2t_chunk_attn / a2t_decode_attn / a2t_evict
- *     allocates memory or synchronises the device; the a2t_read_* calls do
- *     synchronise.
+ *     Nothing in a2t_append / a2t_append_attn / a2t_chunk_attn /
+ *     a2t_decode_attn / a2t_evict / a2t_evict_rule allocates memory (every
+ *     buffer is sized at creation); the a2t_read_* calls synchronise.  The
+ *     calls that open a step (layer 0 or A2T_ALL_LAYERS) stage its metadata
+ *     in one of 16 pinned slots: with 16 earlier steps still queued on the
+ *     device, opening one more waits until the oldest has run (back-pressure,
+ *     not a synchronisation of the whole device).
  *   - A device fault or launch failure poisons the cache: that call and every
  *     later one return A2T_ERR_HIP.
  *   - One host thread at a time per cache.
@@ -52,9 +56,10 @@
  *   (position order).  Eviction removes rows and keeps the survivors in that
  *   order: survivor i moves to slot new_slot[i] = number of survivors before
  *   it.  Physically a stream's rows live in two dense regions per layer:
- *   the "kept" region (rows retained from already-evicted units, in order)
- *   followed, logically, by a ring of the rows of units not yet evicted.
- *   Evicting the oldest units advances the ring head and moves only their
+ *   the "kept" region (rows retained from the part of the stream eviction
+ *   has already passed over, in order) followed, logically, by a ring of the
+ *   newer rows.  Eviction always removes the oldest eligible rows, so it
+ *   advances the ring head past the rows it passes over and moves only their
  *   retained rows into the kept region; a2t_read_layout / a2t_read_kv return
  *   the rows in cache order.
  */
@@ -67,7 +72,7 @@
 extern "C" {
 #endif
 
-#define A2T_ABI_VERSION 1
+#define A2T_ABI_VERSION 2
 #define A2T_ALL_LAYERS (-1)
 
 typedef struct a2t_cache a2t_cache;
@@ -122,6 +127,15 @@ typedef struct a2t_config {
     double attn_scale;      /* softmax scale; 0 selects 1/sqrt(head_dim) */
     int32_t device;         /* HIP device ordinal */
     int32_t reserved;
+    /* Optional caller-owned K and V pools (device memory of `device`, 256-byte
+     * aligned), each L*S*Hkv*(unit_rows + kept_rows)*D elements of the cache
+     * dtype: the ring of every (layer, stream, KV head) first, then the kept
+     * regions ([L][S][Hkv][unit_rows][D] followed by [L][S][Hkv][kept_rows][D]).
+     * Both NULL: the library allocates and frees them.  Both set: the caller
+     * keeps them alive until a2t_cache_destroy returns; the library never frees
+     * them.  Only one set: A2T_ERR_INVALID.  Ignored for host-only caches. */
+    void* k_pool;
+    void* v_pool;
 } a2t_config;
 
 /* Per-stream bookkeeping, for tests and reporting. */
@@ -141,8 +155,10 @@ typedef struct a2t_stream_info {
     int32_t last_evict_pre; /* R before the last eviction that removed rows (-1 if none) */
 } a2t_stream_info;
 
-/* Create a cache.  Allocates every device buffer it will ever use (K/V pools,
- * metadata, attention workspace) and a small pinned-host staging area.
+/* Create a cache.  Allocates every device buffer it will ever use (the K/V
+ * pools unless the caller passes them, metadata, attention workspace), the
+ * host bookkeeping of every stream (sized by unit_rows and max_step_rows) and
+ * a small pinned-host staging area.
  * hip_stream: the hipStream_t to enqueue on (NULL = the default stream).
  * Pools hold L*S*Hkv*(unit_rows+kept_rows)*D elements for each of K and V. */
 int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out);
@@ -220,6 +236,39 @@ int a2t_decode_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_
  * region full). */
 int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* stream_ids, const int32_t* budget,
               int32_t window, int32_t* n_evicted, uint8_t* budget_unmet);
+
+/* Variants of the eviction rule, for ablations and comparisons; a2t_evict
+ * applies A2T_RULE_UNIT.
+ *   A2T_RULE_UNIT         Sec. 3.3: whole units, oldest first, outside the
+ *                         window (see a2t_evict).
+ *   A2T_RULE_ROW          the same eligible rows (ACOUSTIC/DELIM rows of units
+ *                         u <= cur - window), removed one at a time, oldest
+ *                         first, until R <= budget: an ablation of the rule's
+ *                         whole-unit granularity; a unit may lose only part of
+ *                         its rows.
+ *   A2T_RULE_SINK_RECENT  the StreamingLLM comparison (Sec. 2 and Table 1: sink
+ *                         positions plus a recent window): when R > budget,
+ *                         every row except the n_sink oldest and the
+ *                         budget - n_sink newest is removed, whatever its
+ *                         class; window is ignored.  Requires budget >= n_sink;
+ *                         a stream whose kept region holds rows other than its
+ *                         sinks (left there by another rule) cannot switch to
+ *                         it (A2T_ERR_STATE). */
+typedef enum a2t_rule {
+    A2T_RULE_UNIT = 0,
+    A2T_RULE_ROW = 1,
+    A2T_RULE_SINK_RECENT = 2
+} a2t_rule;
+
+/* a2t_evict with a choice of rule (a2t_rule) and, for A2T_RULE_SINK_RECENT,
+ * the sink count (>= 0; ignored by the other rules).  Survivors keep their
+ * positions and order under every rule, and one pass moves the retained rows
+ * of every layer.  Arguments and outputs otherwise as a2t_evict.
+ * Errors: INVALID (unknown rule, n_sink < 0, budget < n_sink under
+ * A2T_RULE_SINK_RECENT, and those of a2t_evict), STATE, CAPACITY. */
+int a2t_evict_rule(a2t_cache* c, int32_t n_streams, const int32_t* stream_ids,
+                   const int32_t* budget, int32_t window, int32_t rule, int32_t n_sink,
+                   int32_t* n_evicted, uint8_t* budget_unmet);
 
 /* Bookkeeping of one stream (host state, no synchronisation). */
 int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out);

@@ -31,11 +31,13 @@ A2T_F32 = 0
 A2T_BF16 = 1
 A2T_ALL_LAYERS = -1
 A2T_FLAG_HOST_ONLY = 1
+A2T_RULE_UNIT, A2T_RULE_ROW, A2T_RULE_SINK_RECENT = 0, 1, 2
 SEG_PREFIX, SEG_ACOUSTIC, SEG_DELIM, SEG_TEXT, SEG_RESPONSE = 0, 1, 2, 3, 4
 
 EXPORTED = (
     "a2t_cache_create", "a2t_cache_destroy", "a2t_set_stream", "a2t_append",
-    "a2t_chunk_attn", "a2t_append_attn", "a2t_decode_attn", "a2t_evict", "a2t_stream_info_get",
+    "a2t_chunk_attn", "a2t_append_attn", "a2t_decode_attn", "a2t_evict", "a2t_evict_rule",
+    "a2t_stream_info_get",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
     "a2t_profile_enable", "a2t_kernel_time", "a2t_profile_reserve", "a2t_status_str",
     "a2t_abi_version", "a2t_distill_create", "a2t_distill_destroy", "a2t_distill_loss",
@@ -50,7 +52,8 @@ class a2t_config(C.Structure):
         ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("dtype", C.c_int32),
         ("unit_rows", C.c_int32), ("kept_rows", C.c_int32), ("max_step_rows", C.c_int32),
         ("flags", C.c_uint32), ("rope_theta", C.c_double), ("attn_scale", C.c_double),
-        ("device", C.c_int32), ("reserved", C.c_int32),
+        ("device", C.c_int32), ("reserved", C.c_int32), ("k_pool", C.c_void_p),
+        ("v_pool", C.c_void_p),
     ]
 
 
@@ -86,6 +89,8 @@ def _load():
                                       P(I32), P(I32), VP, VP]),
         "a2t_decode_attn": (C.c_int, [VP, I32, I32, P(I32), VP, VP]),
         "a2t_evict": (C.c_int, [VP, I32, P(I32), P(I32), I32, P(I32), P(C.c_uint8)]),
+        "a2t_evict_rule": (C.c_int, [VP, I32, P(I32), P(I32), I32, I32, I32, P(I32),
+                                     P(C.c_uint8)]),
         "a2t_stream_info_get": (C.c_int, [VP, I32, P(a2t_stream_info)]),
         "a2t_read_layout": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
         "a2t_read_last_evict": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
@@ -188,9 +193,14 @@ def a2t_status_str(status: int) -> str:
 def a2t_cache_create(n_layers: int, n_streams: int, n_q_heads: int, n_kv_heads: int,
                      head_dim: int, dtype: int, unit_rows: int, kept_rows: int,
                      max_step_rows: int, flags: int = 0, rope_theta: float = 0.0,
-                     attn_scale: float = 0.0, device: int = 0, stream=None) -> Cache:
+                     attn_scale: float = 0.0, device: int = 0, stream=None,
+                     k_pool=None, v_pool=None) -> Cache:
+    """``k_pool``/``v_pool``: optional caller-owned device pools (torch tensors or
+    addresses) of L*S*Hkv*(unit_rows+kept_rows)*D elements each; the caller keeps
+    them alive until a2t_cache_destroy."""
     cfg = a2t_config(n_layers, n_streams, n_q_heads, n_kv_heads, head_dim, dtype, unit_rows,
-                     kept_rows, max_step_rows, flags, rope_theta, attn_scale, device, 0)
+                     kept_rows, max_step_rows, flags, rope_theta, attn_scale, device, 0,
+                     _dev(k_pool, "k_pool"), _dev(v_pool, "v_pool"))
     out = C.c_void_p()
     _check(_lib.a2t_cache_create(C.byref(cfg), _stream_handle(stream), C.byref(out)),
            "a2t_cache_create")
@@ -264,6 +274,18 @@ def a2t_evict(c: Cache, stream_ids: Sequence[int], budget, window: int) -> Tuple
     rc = _lib.a2t_evict(c.ptr, len(ids), _p(ids, C.c_int32), _p(b, C.c_int32), window,
                         _p(n_ev, C.c_int32), _p(unmet, C.c_uint8))
     _check(rc, "a2t_evict")
+    return n_ev, unmet.astype(bool)
+
+
+def a2t_evict_rule(c: Cache, stream_ids: Sequence[int], budget, window: int, rule: int,
+                   n_sink: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    ids = _i32(stream_ids)
+    b = _i32(np.broadcast_to(np.asarray(budget), ids.shape))
+    n_ev = np.zeros(ids.shape, np.int32)
+    unmet = np.zeros(ids.shape, np.uint8)
+    rc = _lib.a2t_evict_rule(c.ptr, len(ids), _p(ids, C.c_int32), _p(b, C.c_int32), window, rule,
+                             n_sink, _p(n_ev, C.c_int32), _p(unmet, C.c_uint8))
+    _check(rc, "a2t_evict_rule")
     return n_ev, unmet.astype(bool)
 
 

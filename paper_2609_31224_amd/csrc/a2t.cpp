@@ -31,6 +31,32 @@ struct UnitRec {
     int32_t evictable;  // ACOUSTIC/DELIM rows among them
 };
 
+// FIFO of the units with rows in the ring, in a buffer sized at creation: every
+// queued unit holds at least one ring row, so unit_rows entries always suffice.
+class UnitQueue {
+public:
+    void init(size_t cap) { buf_.assign(std::max<size_t>(cap, 1), UnitRec{}); }
+    size_t size() const { return n_; }
+    bool empty() const { return n_ == 0; }
+    UnitRec& operator[](size_t i) { return buf_[(h_ + i) % buf_.size()]; }
+    const UnitRec& operator[](size_t i) const { return buf_[(h_ + i) % buf_.size()]; }
+    UnitRec& back() { return (*this)[n_ - 1]; }
+    const UnitRec& back() const { return (*this)[n_ - 1]; }
+    bool full() const { return n_ == buf_.size(); }
+    void push_back(const UnitRec& u) {
+        buf_[(h_ + n_) % buf_.size()] = u;
+        ++n_;
+    }
+    void pop_front(size_t k) {
+        h_ = (h_ + k) % buf_.size();
+        n_ -= k;
+    }
+
+private:
+    std::vector<UnitRec> buf_;
+    size_t h_ = 0, n_ = 0;
+};
+
 struct StreamState {
     int64_t last_pos = -1;
     int32_t cur_unit = -2;          // -2: nothing appended yet
@@ -39,7 +65,8 @@ struct StreamState {
     int32_t head = 0;               // ring head slot
     int32_t ring = 0;               // U
     int32_t peak = 0;
-    std::deque<UnitRec> units;
+    UnitQueue units;
+    std::vector<uint8_t> ring_seg;  // class of every ring slot (host mirror of the device's)
     // open step
     int32_t step_rows = 0;
     int32_t step_slot0 = 0;
@@ -66,6 +93,18 @@ struct ProfEvent {
     hipEvent_t start, stop;
 };
 
+// One stream's eviction, planned on the host.  The device pass moves over the
+// `span` oldest ring rows: it keeps `n_keep` of them (copied to the kept region)
+// and drops `evicted`.
+struct EvictPlan {
+    int n_units = 0;          // whole units popped from the queue
+    int32_t part_rows = 0;    // rows consumed from the next unit (rules that stop inside a unit)
+    int32_t part_evictable = 0;
+    int32_t span = 0, n_keep = 0, evicted = 0, u_last = -2, R_pre = 0;
+    int32_t sink = -1;        // A2T_RULE_SINK_RECENT: the sink count (rows kept by index)
+    bool unmet = false;
+};
+
 }  // namespace
 
 struct a2t_cache {
@@ -87,12 +126,15 @@ struct a2t_cache {
     std::vector<uint32_t> seen;      // stream id -> call stamp
     uint32_t stamp = 0;
     std::vector<int32_t> tmp_nq, tmp_row0, tmp_in0;
+    std::vector<EvictPlan> evict_plans;
+    bool own_pools = true;           // false: the K/V pools belong to the caller
     // attention tuning
     int target_wgs = 1024;
     int force_splits = 0;
     // the last split plan (every layer of a step plans the same resident counts)
     int plan_n = 0;
     int plan_force = -1;
+    int64_t plan_limit = -1;
     std::vector<int> plan_tiles, plan_splits, plan_tmp, plan_order;
     std::vector<int64_t> plan_heap;
     bool force_valu = false;
@@ -259,15 +301,15 @@ int64_t launch_makespan(int n, const int* tiles, const int* splits, int Hkv, int
 }
 
 void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_per_split,
-                 int* splits) {
+                 int* splits, int64_t ws_limit) {
     // every layer of a step plans the same resident counts: reuse the last plan
     // while its partials fit the workspace (query counts may differ)
     if (c->plan_n == n && std::equal(tiles, tiles + n, c->plan_tiles.begin()) &&
-        c->plan_force == c->force_splits) {
+        c->plan_force == c->force_splits && c->plan_limit == ws_limit) {
         int64_t ws = 0;
         for (int i = 0; i < n; ++i)
             if (c->plan_splits[i] > 1) ws += c->plan_splits[i] * floats_per_split[i];
-        if (ws <= c->dev.ws_floats) {
+        if (ws <= ws_limit) {
             std::copy(c->plan_splits.begin(), c->plan_splits.begin() + n, splits);
             return;
         }
@@ -287,7 +329,7 @@ void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_pe
                 w += (int64_t)sp[i] * Hkv;
                 if (sp[i] > 1) ws += sp[i] * floats_per_split[i];
             }
-            if (ws > c->dev.ws_floats) continue;
+            if (ws > ws_limit) continue;
             const int64_t cost = launch_makespan(n, tiles, sp.data(), Hkv, c->target_wgs,
                                                  c->plan_order, c->plan_heap);
             if (cost < best_cost || (cost == best_cost && w < best_w)) {
@@ -303,6 +345,7 @@ void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_pe
         } else {
             c->plan_n = n;
             c->plan_force = c->force_splits;
+            c->plan_limit = ws_limit;
             c->plan_tiles.assign(tiles, tiles + n);
             c->plan_splits.assign(splits, splits + n);
             return;
@@ -318,11 +361,12 @@ void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_pe
             if (splits[i] > 1) ws += splits[i] * floats_per_split[i];
             mx = std::max(mx, splits[i]);
         }
-        if (ws <= c->dev.ws_floats || mx == 1) break;
+        if (ws <= ws_limit || mx == 1) break;
         for (int i = 0; i < n; ++i) splits[i] = std::max(1, splits[i] / 2);
     }
     c->plan_n = n;
     c->plan_force = c->force_splits;
+    c->plan_limit = ws_limit;
     c->plan_tiles.assign(tiles, tiles + n);
     c->plan_splits.assign(splits, splits + n);
 }
@@ -345,7 +389,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         max_rows = std::max(max_rows, n_q[i]);
         floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
     }
-    plan_splits(c, n, tiles, floats, nsplit);
+    plan_splits(c, n, tiles, floats, nsplit, c->dev.ws_floats);
     // descriptors in order of falling tiles per split: the dispatcher starts the
     // longest workgroups first
     int ord[kMaxDesc];
@@ -427,8 +471,12 @@ int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* i
 }
 
 void free_device(a2t_cache* c) {
-    void* ptrs[] = {c->dev.k_unit, c->dev.v_unit, c->dev.k_kept, c->dev.v_kept,
-                    c->dev.unit_pos, c->dev.unit_uid, c->dev.unit_seg, c->dev.kept_pos,
+    if (c->own_pools) {
+        // a library-allocated pool is one allocation per tensor: ring, then kept regions
+        if (c->dev.k_unit) (void)hipFree(c->dev.k_unit);
+        if (c->dev.v_unit) (void)hipFree(c->dev.v_unit);
+    }
+    void* ptrs[] = {c->dev.unit_pos, c->dev.unit_uid, c->dev.unit_seg, c->dev.kept_pos,
                     c->dev.kept_uid, c->dev.kept_seg, c->dev.rope, c->dev.ev_mask,
                     c->dev.ev_slot, c->dev.ws};
     for (void* p : ptrs)
@@ -476,6 +524,9 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     if (k.max_step_rows < 1 || k.max_step_rows > 1024) return A2T_ERR_INVALID;
     if (k.rope_theta < 0 || k.attn_scale < 0) return A2T_ERR_INVALID;
     if ((int64_t)k.unit_rows + k.kept_rows > (int64_t)1 << 30) return A2T_ERR_INVALID;
+    if ((k.k_pool == nullptr) != (k.v_pool == nullptr)) return A2T_ERR_INVALID;
+    if ((reinterpret_cast<uintptr_t>(k.k_pool) | reinterpret_cast<uintptr_t>(k.v_pool)) & 255u)
+        return A2T_ERR_INVALID;
 
     a2t_cache* c = new (std::nothrow) a2t_cache();
     if (!c) return A2T_ERR_OOM;
@@ -485,11 +536,18 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     c->host_only = (k.flags & A2T_FLAG_HOST_ONLY) != 0;
     c->stream = static_cast<hipStream_t>(hip_stream);
     c->ss.resize(k.n_streams);
-    for (auto& s : c->ss) s.appended.assign(k.n_layers, 1);
+    for (auto& s : c->ss) {
+        s.appended.assign(k.n_layers, 1);
+        s.units.init((size_t)k.unit_rows);
+        s.ring_seg.assign((size_t)k.unit_rows, 0);
+        s.step_seg.reserve((size_t)k.max_step_rows);
+        s.step_pos.reserve((size_t)k.max_step_rows);
+    }
     c->seen.assign(k.n_streams, 0u);
     c->tmp_nq.assign(k.n_streams, 0);
     c->tmp_row0.assign(k.n_streams, 0);
     c->tmp_in0.assign(k.n_streams, 0);
+    c->evict_plans.assign(k.n_streams, EvictPlan{});
     {
         // one workgroup of the attention kernel per CU: a launch runs in rounds of CU count
         int cus = 0;
@@ -500,6 +558,9 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     }
     c->force_splits = std::max(0, env_int("A2T_SPLITS", 0));
     c->force_valu = env_flag("A2T_FORCE_VALU");
+    // the split planner's scratch, so that no attention call allocates
+    for (auto* v : {&c->plan_tiles, &c->plan_splits, &c->plan_tmp, &c->plan_order}) v->reserve(kMaxDesc);
+    c->plan_heap.reserve((size_t)c->target_wgs);
 
     DevState& d = c->dev;
     d.L = k.n_layers;
@@ -542,10 +603,19 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
         if (!ok) return;
         if (hipMalloc(p, std::max<int64_t>(bytes, 256)) != hipSuccess) ok = false;
     };
-    alloc(&d.k_unit, lsh * k.unit_rows);
-    alloc(&d.v_unit, lsh * k.unit_rows);
-    alloc(&d.k_kept, lsh * std::max(1, k.kept_rows));
-    alloc(&d.v_kept, lsh * std::max(1, k.kept_rows));
+    // K and V pools: [L][S][Hkv][unit_rows][D] ring, then [L][S][Hkv][kept_rows][D] kept
+    c->own_pools = (k.k_pool == nullptr);
+    if (c->own_pools) {
+        alloc(&d.k_unit, lsh * tot);
+        alloc(&d.v_unit, lsh * tot);
+    } else {
+        d.k_unit = k.k_pool;
+        d.v_unit = k.v_pool;
+    }
+    if (ok) {
+        d.k_kept = static_cast<char*>(d.k_unit) + lsh * k.unit_rows;
+        d.v_kept = static_cast<char*>(d.v_unit) + lsh * k.unit_rows;
+    }
     alloc((void**)&d.unit_pos, S * k.unit_rows * 4);
     alloc((void**)&d.unit_uid, S * k.unit_rows * 4);
     alloc((void**)&d.unit_seg, S * k.unit_rows);
@@ -641,6 +711,8 @@ static int append_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int
             if (u == -1 && s.cur_unit >= 0) return A2T_ERR_POS;
             if (s.cur_unit != -2 && u < s.cur_unit) return A2T_ERR_POS;
             if ((int64_t)s.ring + n > k.unit_rows) return A2T_ERR_CAPACITY;
+            // a new unit needs a queue entry (never short: every entry holds a ring row)
+            if (!(s.units.size() && s.units.back().unit == u) && s.units.full()) return A2T_ERR_CAPACITY;
         } else {
             if (s.step_rows == 0 || s.appended[layer]) return A2T_ERR_STATE;
             if (n != s.step_rows) return A2T_ERR_POS;
@@ -666,13 +738,14 @@ static int append_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int
             for (int r = 0; r < n; ++r) ev += is_evictable(seg[off + r]);
             s.step_rows = n;
             s.step_slot0 = (s.head + s.ring) % k.unit_rows;
+            for (int r = 0; r < n; ++r) s.ring_seg[(s.step_slot0 + r) % k.unit_rows] = seg[off + r];
             s.step_seg.assign(seg + off, seg + off + n);
             s.step_pos.assign(pos + off, pos + off + n);
             s.step_unit = u;
             std::fill(s.appended.begin(), s.appended.end(), layer == A2T_ALL_LAYERS ? 1 : 0);
             if (layer == 0) s.appended[0] = 1;
             s.ring += n;
-            if (!s.units.empty() && s.units.back().unit == u) {
+            if (s.units.size() && s.units.back().unit == u) {
                 s.units.back().rows += n;
                 s.units.back().evictable += ev;
             } else {
@@ -809,46 +882,136 @@ int a2t_decode_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_
     return attn_common(c, layer, n_streams, ids, nullptr, q, o, true);
 }
 
-int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t* budget,
-              int32_t window, int32_t* n_evicted, uint8_t* budget_unmet) {
+}  // extern "C"
+
+namespace {
+
+// Number of ACOUSTIC/DELIM rows among `n` ring rows starting at `slot`.
+int32_t evictable_in(const StreamState& s, int32_t slot, int32_t n, int32_t ring_rows) {
+    int32_t e = 0;
+    for (int32_t r = 0; r < n; ++r) {
+        int32_t x = slot + r;
+        if (x >= ring_rows) x -= ring_rows;
+        e += is_evictable(s.ring_seg[x]);
+    }
+    return e;
+}
+
+// Sec. 3.3 and its variants, planned from the host mirror of one stream.
+// A2T_RULE_UNIT: while R > B, the oldest unit outside the W most recent units
+// that still holds acoustic/structural rows loses all of them.  A2T_RULE_ROW:
+// the same rows one at a time, so the last unit touched may lose only part of
+// them.  A2T_RULE_SINK_RECENT: everything but the n_sink oldest and the
+// B - n_sink newest rows.
+int plan_stream(const a2t_cache* c, const StreamState& s, int rule, int32_t budget,
+                int32_t window, int32_t n_sink, EvictPlan& p) {
+    p = EvictPlan{};
+    const int32_t ring_rows = c->cfg.unit_rows;
+    int32_t R = s.resident();
+    p.R_pre = R;
+    if (rule == A2T_RULE_SINK_RECENT) {
+        if (R > budget) {
+            if (s.kept > n_sink) return A2T_ERR_STATE;   // the kept region holds non-sink rows
+            const int32_t sinks_left = n_sink - s.kept;  // the oldest ring rows are still sinks
+            p.sink = n_sink;
+            p.evicted = R - budget;
+            p.n_keep = sinks_left;
+            p.span = sinks_left + p.evicted;             // <= ring, since budget >= n_sink
+            int32_t rest = p.span;
+            size_t t = 0;
+            while (t < s.units.size() && rest >= s.units[t].rows) {
+                rest -= s.units[t].rows;
+                p.u_last = s.units[t].unit;
+                ++t;
+            }
+            p.n_units = (int)t;
+            if (rest > 0) {
+                p.part_rows = rest;
+                p.part_evictable = evictable_in(s, (s.head + p.span - rest) % ring_rows, rest, ring_rows);
+                p.u_last = s.units[t].unit;
+            }
+            R = budget;
+        }
+        p.unmet = R > budget;
+        return A2T_OK;
+    }
+    const int64_t limit = (int64_t)s.cur_unit - window;
+    if (rule == A2T_RULE_ROW) {
+        // walk the ring from its head: every eligible ACOUSTIC/DELIM row goes, oldest
+        // first, until R <= B; units whose remaining rows hold none are skipped whole
+        const int32_t need = R - budget;
+        int32_t x = 0;            // ring offset of the next row
+        for (size_t t = 0; p.evicted < need && t < s.units.size(); ++t) {
+            const UnitRec& u = s.units[t];
+            if ((int64_t)u.unit > limit) break;
+            if (u.evictable == 0) {
+                x += u.rows;
+                continue;
+            }
+            int32_t ev = 0;
+            for (int32_t r = 0; r < u.rows && ev < u.evictable && p.evicted < need; ++r) {
+                if (is_evictable(s.ring_seg[(s.head + x + r) % ring_rows])) {
+                    ++ev;
+                    ++p.evicted;
+                    p.span = x + r + 1;     // the pass ends at the newest evicted row
+                    p.u_last = u.unit;
+                }
+            }
+            x += u.rows;
+        }
+        // units wholly inside the pass leave the queue; the next one loses its first rows
+        int32_t rest = p.span;
+        size_t t = 0;
+        while (t < s.units.size() && rest > 0 && rest >= s.units[t].rows) rest -= s.units[t++].rows;
+        p.n_units = (int)t;
+        if (rest > 0) {
+            p.part_rows = rest;
+            p.part_evictable = evictable_in(s, (s.head + p.span - rest) % ring_rows, rest, ring_rows);
+        }
+        p.n_keep = p.span - p.evicted;
+        R -= p.evicted;
+        p.unmet = R > budget;
+        return A2T_OK;
+    }
+    size_t next = 0;
+    while (R > budget) {
+        size_t j = next;
+        while (j < s.units.size() && s.units[j].evictable == 0) ++j;
+        if (j >= s.units.size() || (int64_t)s.units[j].unit > limit) break;
+        for (size_t t = next; t <= j; ++t) {
+            p.span += s.units[t].rows;
+            p.n_keep += s.units[t].rows - s.units[t].evictable;
+        }
+        p.evicted += s.units[j].evictable;
+        R -= s.units[j].evictable;
+        p.u_last = s.units[j].unit;
+        next = j + 1;
+    }
+    p.n_units = (int)next;
+    p.unmet = R > budget;
+    return A2T_OK;
+}
+
+int evict_impl(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t* budget,
+               int32_t window, int32_t rule, int32_t n_sink, int32_t* n_evicted,
+               uint8_t* budget_unmet) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
     int rc = check_streams(c, n_streams, ids);
     if (rc) return rc;
     if (!budget || window < 0) return A2T_ERR_INVALID;
-    struct Plan {
-        int n_units = 0;      // units popped from the ring queue (passed over or evicted)
-        int32_t span = 0, n_keep = 0, evicted = 0, u_last = -2, R_pre = 0;
-        bool unmet = false;
-    };
-    std::vector<Plan> plans(n_streams);
+    if (rule != A2T_RULE_UNIT && rule != A2T_RULE_ROW && rule != A2T_RULE_SINK_RECENT)
+        return A2T_ERR_INVALID;
+    if (n_sink < 0) return A2T_ERR_INVALID;
+    EvictPlan* plans = c->evict_plans.data();   // sized n_streams at creation
     for (int i = 0; i < n_streams; ++i) {
         if (budget[i] < 0) return A2T_ERR_INVALID;
+        if (rule == A2T_RULE_SINK_RECENT && budget[i] < n_sink) return A2T_ERR_INVALID;
         const StreamState& s = c->ss[ids[i]];
         if (!s.step_complete()) return A2T_ERR_STATE;
-        // Sec. 3.3: while R > B, evict the oldest unit outside the W most recent
-        // units that still holds acoustic/structural rows.
-        Plan& p = plans[i];
-        int32_t R = s.resident();
-        p.R_pre = R;
-        const int64_t limit = (int64_t)s.cur_unit - window;
-        size_t next = 0;
-        while (R > budget[i]) {
-            size_t j = next;
-            while (j < s.units.size() && s.units[j].evictable == 0) ++j;
-            if (j >= s.units.size() || (int64_t)s.units[j].unit > limit) break;
-            for (size_t t = next; t <= j; ++t) {
-                p.span += s.units[t].rows;
-                p.n_keep += s.units[t].rows - s.units[t].evictable;
-            }
-            p.evicted += s.units[j].evictable;
-            R -= s.units[j].evictable;
-            p.u_last = s.units[j].unit;
-            next = j + 1;
-        }
-        p.n_units = (int)next;
-        p.unmet = R > budget[i];
-        if ((int64_t)s.kept + p.n_keep > c->cfg.kept_rows) return A2T_ERR_CAPACITY;
+        rc = plan_stream(c, s, rule, budget[i], window, n_sink, plans[i]);
+        if (rc) return rc;
+        if ((int64_t)s.kept + plans[i].n_keep > c->cfg.kept_rows) return A2T_ERR_CAPACITY;
     }
     // device work for the streams that evict
     if (!c->host_only) {
@@ -865,10 +1028,10 @@ int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t
             return e == hipSuccess ? A2T_OK : hip_fail(c);
         };
         for (int i = 0; i < n_streams; ++i) {
-            const Plan& p = plans[i];
+            const EvictPlan& p = plans[i];
             if (p.evicted == 0) continue;
             const StreamState& s = c->ss[ids[i]];
-            eb.d[eb.count++] = EvictDesc{ids[i], s.kept, s.head, p.R_pre, p.span, p.u_last, p.n_keep};
+            eb.d[eb.count++] = EvictDesc{ids[i], s.kept, s.head, p.R_pre, p.span, p.u_last, p.n_keep, p.sink};
             if (eb.count == kMaxDesc && (rc = flush())) return rc;
         }
         if ((rc = flush())) return rc;
@@ -876,9 +1039,13 @@ int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t
     // host state
     for (int i = 0; i < n_streams; ++i) {
         StreamState& s = c->ss[ids[i]];
-        const Plan& p = plans[i];
+        const EvictPlan& p = plans[i];
         if (p.evicted > 0) {
-            for (int t = 0; t < p.n_units; ++t) s.units.pop_front();
+            s.units.pop_front((size_t)p.n_units);
+            if (p.part_rows) {
+                s.units[0].rows -= p.part_rows;
+                s.units[0].evictable -= p.part_evictable;
+            }
             s.kept += p.n_keep;
             s.head = (int32_t)(((int64_t)s.head + p.span) % c->cfg.unit_rows);
             s.ring -= p.span;
@@ -894,6 +1061,21 @@ int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t
         if (budget_unmet) budget_unmet[i] = p.unmet ? 1 : 0;
     }
     return A2T_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int a2t_evict(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t* budget,
+              int32_t window, int32_t* n_evicted, uint8_t* budget_unmet) {
+    return evict_impl(c, n_streams, ids, budget, window, A2T_RULE_UNIT, 0, n_evicted, budget_unmet);
+}
+
+int a2t_evict_rule(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t* budget,
+                   int32_t window, int32_t rule, int32_t n_sink, int32_t* n_evicted,
+                   uint8_t* budget_unmet) {
+    return evict_impl(c, n_streams, ids, budget, window, rule, n_sink, n_evicted, budget_unmet);
 }
 
 int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out) {

@@ -23,10 +23,10 @@ constexpr int kMergeRows = 4;
 
 // Device-side buffers of a cache and its shape.
 struct DevState {
-    void* k_unit;   // [L][S][Hkv][unit_rows][D]  rotated keys of not-yet-evicted units (ring)
-    void* v_unit;   // [L][S][Hkv][unit_rows][D]
-    void* k_kept;   // [L][S][Hkv][kept_rows][D]  rows retained from evicted units, in order
-    void* v_kept;   // [L][S][Hkv][kept_rows][D]
+    void* k_unit;   // [L][S][Hkv][unit_rows][D]  rotated keys of the rows eviction has not
+    void* v_unit;   //                             passed over yet (ring); V likewise
+    void* k_kept;   // [L][S][Hkv][kept_rows][D]  rows retained from the part eviction has
+    void* v_kept;   //                             passed over, in order (right after the ring)
     int32_t* unit_pos;  // [S][unit_rows] metadata of ring slots
     int32_t* unit_uid;
     uint8_t* unit_seg;
@@ -114,9 +114,13 @@ struct EvictDesc {
     int32_t kept;      // T before eviction
     int32_t head;      // ring head before eviction
     int32_t R_pre;     // resident rows before eviction
-    int32_t span;      // ring rows passed over (all rows of units up to u_last)
-    int32_t u_last;    // newest evicted unit id
+    int32_t span;      // oldest ring rows passed over (up to and including the last evicted
+                       // row, or every row of the units up to u_last)
+    int32_t u_last;    // unit id of the newest evicted row
     int32_t n_keep;    // rows of the span that are retained (moved to the kept region)
+    int32_t sink;      // >= 0: the span's rows with cache index < sink are kept, every
+                       // other one is evicted (sink + recent rule); -1: retained rows
+                       // are those of a class that is never evicted
 };
 template <int N>
 struct EvictBatchT {

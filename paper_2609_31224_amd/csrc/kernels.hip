@@ -1027,9 +1027,13 @@ __global__ __launch_bounds__(256) void evict_kernel(DevState st, BT b) {
         if (in) {
             slot = d.head + x;
             if (slot >= st.unit_rows) slot -= st.unit_rows;
-            const uint8_t sg = st.unit_seg[mb + slot];
-            const int uid = st.unit_uid[mb + slot];
-            keep = !((sg == kSegAcoustic || sg == kSegDelim) && uid <= d.u_last);
+            if (d.sink >= 0) {
+                keep = d.kept + x < d.sink;
+            } else {
+                const uint8_t sg = st.unit_seg[mb + slot];
+                const int uid = st.unit_uid[mb + slot];
+                keep = !((sg == kSegAcoustic || sg == kSegDelim) && uid <= d.u_last);
+            }
         }
         const uint64_t bal = __ballot(keep);
         const int below = __popcll(bal & ((1ull << lane) - 1ull));

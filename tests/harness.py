@@ -73,10 +73,18 @@ class Lockstep:
 
     def __init__(self, cfg, seed, specs, *, layers_checked, n_layers, budgets, window,
                  unit_rows, kept_rows, max_step, tol, dtype=None, check_kv_every=1,
-                 all_layers_append=False, query_rows=None, fused=False):
+                 all_layers_append=False, query_rows=None, fused=False, rule=None, n_sink=0):
         from oracle.cache import OracleCache
+        from oracle.policy import EvictRule
         import paper_2609_31224_amd as a2t
         self.a2t = a2t
+        # eviction rule: None = a2t_evict (the paper's whole-unit rule), else
+        # "unit" / "row" / "sink_recent" through a2t_evict_rule
+        self.rule = rule
+        self.n_sink = n_sink
+        self.oracle_rule = EvictRule(rule or "unit", n_sink)
+        self.lib_rule = {None: None, "unit": a2t.A2T_RULE_UNIT, "row": a2t.A2T_RULE_ROW,
+                         "sink_recent": a2t.A2T_RULE_SINK_RECENT}[rule]
         self.cfg, self.seed, self.specs = cfg, seed, specs
         self.dtype = dtype or cfg.dtype
         self.layers_checked = list(layers_checked)
@@ -193,9 +201,13 @@ class Lockstep:
             return
         ev_ids = [i for i, _ in ev_act]
         budgets = [self.budgets[i] for i in ev_ids]
-        n_ev, unmet = a2t.a2t_evict(self.cache, ev_ids, budgets, self.window)
+        if self.lib_rule is None:
+            n_ev, unmet = a2t.a2t_evict(self.cache, ev_ids, budgets, self.window)
+        else:
+            n_ev, unmet = a2t.a2t_evict_rule(self.cache, ev_ids, budgets, self.window,
+                                             self.lib_rule, self.n_sink)
         for j, (i, st) in enumerate(ev_act):
-            rec = self.oracles[i].evict(self.budgets[i], self.window)
+            rec = self.oracles[i].evict(self.budgets[i], self.window, self.oracle_rule)
             if int(n_ev[j]) != rec.n_evicted or bool(unmet[j]) != rec.plan.budget_unmet:
                 raise Mismatch(f"step {t} stream {i}: evicted {n_ev[j]}/{rec.n_evicted} "
                                f"unmet {unmet[j]}/{rec.plan.budget_unmet}")

@@ -37,7 +37,7 @@ def test_every_declared_call_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert a2t.a2t_abi_version() == 1
+    assert a2t.a2t_abi_version() == 2
     assert a2t.a2t_status_str(0) == "ok"
     for s in range(-7, 0):
         assert a2t.a2t_status_str(s) != "unknown status"
@@ -76,6 +76,12 @@ def test_create_validation():
         kw = dict(base, **b)
         with pytest.raises(a2t.A2TError) as e:
             a2t.a2t_cache_create(**kw)
+        assert e.value.status == a2t.A2T_ERR_INVALID
+    # caller-owned pools: both or neither, 256-byte aligned
+    for pools in (dict(k_pool=1 << 20), dict(v_pool=1 << 20), dict(k_pool=(1 << 20) + 64,
+                                                                   v_pool=1 << 20)):
+        with pytest.raises(a2t.A2TError) as e:
+            a2t.a2t_cache_create(**dict(base, **pools))
         assert e.value.status == a2t.A2T_ERR_INVALID
 
 
@@ -141,14 +147,43 @@ def test_evict_errors():
     assert _status(a2t.a2t_evict, c2, [0], [0], 0) == a2t.A2T_ERR_STATE   # layer 1 not appended
 
 
-def _library_trace(spec, budget, window, unit_rows, kept_rows, max_step):
+def test_evict_rule_errors():
+    c = host_cache(unit_rows=64, kept_rows=8, layers=1)
+    a2t.a2t_append(c, 0, [0], [3], None, None, [1, 3, 3], [0, 1, 2], [0])
+    before = a2t.a2t_stream_info_get(c, 0)
+    assert _status(a2t.a2t_evict_rule, c, [0], [2], 0, 3) == a2t.A2T_ERR_INVALID      # no such rule
+    assert _status(a2t.a2t_evict_rule, c, [0], [2], 0, 2, -1) == a2t.A2T_ERR_INVALID  # n_sink < 0
+    assert _status(a2t.a2t_evict_rule, c, [0], [2], 0, 2, 3) == a2t.A2T_ERR_INVALID   # budget < n_sink
+    assert a2t.a2t_stream_info_get(c, 0) == before
+    # the whole-unit rule leaves transcript rows in the kept region: the sink
+    # rule cannot take over the stream while those rows would have to go
+    a2t.a2t_append(c, 0, [0], [3], None, None, [1, 3, 3], [3, 4, 5], [1])
+    n_ev, _ = a2t.a2t_evict(c, [0], [4], 1)
+    assert n_ev[0] == 1 and a2t.a2t_stream_info_get(c, 0)["kept"] == 2
+    a2t.a2t_append(c, 0, [0], [2], None, None, [1, 1], [6, 7], [2])
+    before = a2t.a2t_stream_info_get(c, 0)
+    assert _status(a2t.a2t_evict_rule, c, [0], [3], 0, a2t.A2T_RULE_SINK_RECENT, 1) == \
+        a2t.A2T_ERR_STATE
+    assert a2t.a2t_stream_info_get(c, 0) == before
+    # with enough sinks to cover the kept region it proceeds
+    n_ev, _ = a2t.a2t_evict_rule(c, [0], [3], 0, a2t.A2T_RULE_SINK_RECENT, 2)
+    assert n_ev[0] == 4 and a2t.a2t_stream_info_get(c, 0)["resident"] == 3
+
+
+def _evict(c, budget, window, rule):
+    if rule is None:
+        return a2t.a2t_evict(c, [0], [budget], window)
+    return a2t.a2t_evict_rule(c, [0], [budget], window, *rule)
+
+
+def _library_trace(spec, budget, window, unit_rows, kept_rows, max_step, rule=None):
     c = host_cache(unit_rows=unit_rows, kept_rows=kept_rows, max_step=max_step, layers=1)
     rows = []
     for st in spec.steps:
         append_all(c, 0, st)
         pre = a2t.a2t_stream_info_get(c, 0)["resident"]
         moved0 = a2t.a2t_stream_info_get(c, 0)["moved_total"]
-        n_ev, unmet = a2t.a2t_evict(c, [0], [budget], window)
+        n_ev, unmet = _evict(c, budget, window, rule)
         info = a2t.a2t_stream_info_get(c, 0)
         rows.append((pre, int(n_ev[0]), bool(unmet[0]), info["resident"], info["last_evicted_unit"],
                      info["moved_total"] - moved0))
@@ -157,11 +192,23 @@ def _library_trace(spec, budget, window, unit_rows, kept_rows, max_step):
     return rows, peak
 
 
-def _compare(spec, budget, window):
+RULES = {None: None, "row": (a2t.A2T_RULE_ROW, 0), "sink": (a2t.A2T_RULE_SINK_RECENT, 4)}
+
+
+def _oracle_rule(rule):
+    from oracle.policy import EvictRule
+    if rule is None or rule[0] == a2t.A2T_RULE_UNIT:
+        return EvictRule("unit")
+    if rule[0] == a2t.A2T_RULE_ROW:
+        return EvictRule("row")
+    return EvictRule("sink_recent", rule[1])
+
+
+def _compare(spec, budget, window, rule=None):
     total = spec.total_rows()
     rows, peak = _library_trace(spec, budget, window, total + 1, total + 1,
-                                max(st.n for st in spec.steps))
-    tr = replay_metadata(spec, budget, window)
+                                max(st.n for st in spec.steps), rule)
+    tr = replay_metadata(spec, budget, window, rule=_oracle_rule(rule))
     for (pre, n_ev, unmet, post, last_u, moved), t in zip(rows, tr.steps):
         assert pre == t.n_pre
         # rows copied into the kept region = rows joining the oracle's retained prefix
@@ -214,3 +261,45 @@ def test_planner_golden_and_edge_streams():
     ]
     for units, B, W, prefix in shapes:
         _compare(tiny_stream(units, prefix=prefix, pos_gap=2), B, W)
+
+
+# --------------------------------------------- the rule variants against the oracle
+@pytest.mark.parametrize("rule", ["row", "sink"])
+@pytest.mark.parametrize("seed", range(4))
+def test_planner_rule_variants_config0(rule, seed):
+    cfg = CONFIGS[0]
+    budget = cfg.budget if rule == "row" else 4 + 120
+    _compare(make_workload(cfg, seed=seed).streams[0], budget, cfg.window, RULES[rule])
+
+
+@pytest.mark.parametrize("rule", ["row", "sink"])
+def test_planner_rule_variants_config1(rule):
+    cfg = CONFIGS[1]
+    budget = cfg.budget if rule == "row" else 4 + 2000
+    _compare(make_workload(cfg).streams[0], budget, cfg.window, RULES[rule])
+
+
+@pytest.mark.parametrize("rule", ["row", "sink"])
+def test_planner_rule_variants_batched_workloads(rule):
+    w = make_workload(2)
+    for spec in w.streams[:4]:
+        budget = spec.budget if rule == "row" else 4 + spec.budget // 2
+        _compare(spec, budget, w.config.window, RULES[rule])
+    w = make_workload(3, n_streams=1)
+    budget = w.streams[0].budget if rule == "row" else 4 + 2000
+    _compare(w.streams[0], budget, w.config.window, RULES[rule])
+
+
+@pytest.mark.parametrize("rule", [(a2t.A2T_RULE_ROW, 0), (a2t.A2T_RULE_SINK_RECENT, 0),
+                                  (a2t.A2T_RULE_SINK_RECENT, 1), (a2t.A2T_RULE_SINK_RECENT, 3)])
+def test_planner_rule_variants_edge_streams(rule):
+    shapes = [
+        ([[1, 1, 2, 3, 2]] * 6, 10, 1, 2),
+        ([[1, 1, 3]] * 8, 3, 2, 0),
+        ([[1, 1, 2, 2], [4], [1, 1, 3], [4], [4]], 6, 1, 0),
+        ([[1, 3]] * 5, 3, 0, 0),
+        ([[3, 3], [1, 1], [3], [1, 2, 2, 1]] * 3, 4, 1, 3),
+        ([[2, 3, 3, 3, 1, 1]] * 5, 7, 1, 1),
+    ]
+    for units, B, W, prefix in shapes:
+        _compare(tiny_stream(units, prefix=prefix, pos_gap=2), max(B, rule[1]), W, rule)
