@@ -109,6 +109,10 @@ typedef enum a2t_seg {
 #define A2T_FLAG_HOST_ONLY 1u  /* no device: bookkeeping and eviction planning only
                                   (append/evict update the host state; attention and
                                   device reads return A2T_ERR_NODEV) */
+#define A2T_FLAG_NO_WORKSPACE 2u  /* allocate no key-split workspace (256 MiB by default):
+                                  the attention calls then run one split per stream,
+                                  except a2t_append_attn_noalloc, which splits into the
+                                  library's fixed array */
 
 typedef struct a2t_config {
     int32_t n_layers;       /* L >= 1 */
@@ -215,6 +219,27 @@ int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_
                     const int32_t* n_rows, const void* k, const void* v, const uint8_t* seg,
                     const int32_t* pos, const int32_t* unit_id, const int32_t* n_q,
                     const void* q, void* o);
+
+/* a2t_append_attn for callers that cannot allocate memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  Same
+ * arguments, results and cache contents as a2t_append_attn; the key-split
+ * partials go to a fixed 16 MiB device array of the library (one per GPU, held
+ * until the process ends) instead of the cache's workspace, so it also works
+ * on a cache created with A2T_FLAG_NO_WORKSPACE.  Splits are planned as
+ * a2t_append_attn plans them without a workspace limit; a call whose launch
+ * would write more than 16 MiB of partials (4,194,304 floats; a stream's
+ * partials are splits x n_q x n_q_heads x (head_dim + 2) floats, about 8 MiB
+ * for 22 query rows x 32 heads x head dim 128 at ~4,100 resident rows) is
+ * rejected with A2T_ERR_CAPACITY before anything changes.  Every call on a GPU
+ * shares that GPU's array: calls that overlap on one GPU (two caches on
+ * different streams, or two host threads) race and must be serialised by the
+ * caller; calls in order on one stream are safe.  Its launches are never timed
+ * (a2t_profile_enable does not apply).  Errors: those of a2t_append_attn,
+ * CAPACITY as above, NODEV if the array is not available on the device. */
+int a2t_append_attn_noalloc(a2t_cache* c, int32_t layer, int32_t n_streams,
+                            const int32_t* stream_ids, const int32_t* n_rows, const void* k,
+                            const void* v, const uint8_t* seg, const int32_t* pos,
+                            const int32_t* unit_id, const int32_t* n_q, const void* q, void* o);
 
 /* Decode attention while speaking: one query per stream, the stream's newest
  * row (Sec. 3.1: response tokens are decoded one by one over the cache).

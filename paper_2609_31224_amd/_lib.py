@@ -31,12 +31,14 @@ A2T_F32 = 0
 A2T_BF16 = 1
 A2T_ALL_LAYERS = -1
 A2T_FLAG_HOST_ONLY = 1
+A2T_FLAG_NO_WORKSPACE = 2
 A2T_RULE_UNIT, A2T_RULE_ROW, A2T_RULE_SINK_RECENT = 0, 1, 2
 SEG_PREFIX, SEG_ACOUSTIC, SEG_DELIM, SEG_TEXT, SEG_RESPONSE = 0, 1, 2, 3, 4
 
 EXPORTED = (
     "a2t_cache_create", "a2t_cache_destroy", "a2t_set_stream", "a2t_append",
-    "a2t_chunk_attn", "a2t_append_attn", "a2t_decode_attn", "a2t_evict", "a2t_evict_rule",
+    "a2t_chunk_attn", "a2t_append_attn", "a2t_append_attn_noalloc", "a2t_decode_attn",
+    "a2t_evict", "a2t_evict_rule",
     "a2t_stream_info_get",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
     "a2t_profile_enable", "a2t_kernel_time", "a2t_profile_reserve", "a2t_status_str",
@@ -87,6 +89,8 @@ def _load():
         "a2t_chunk_attn": (C.c_int, [VP, I32, I32, P(I32), P(I32), VP, VP]),
         "a2t_append_attn": (C.c_int, [VP, I32, I32, P(I32), P(I32), VP, VP, P(C.c_uint8), P(I32),
                                       P(I32), P(I32), VP, VP]),
+        "a2t_append_attn_noalloc": (C.c_int, [VP, I32, I32, P(I32), P(I32), VP, VP, P(C.c_uint8),
+                                              P(I32), P(I32), P(I32), VP, VP]),
         "a2t_decode_attn": (C.c_int, [VP, I32, I32, P(I32), VP, VP]),
         "a2t_evict": (C.c_int, [VP, I32, P(I32), P(I32), I32, P(I32), P(C.c_uint8)]),
         "a2t_evict_rule": (C.c_int, [VP, I32, P(I32), P(I32), I32, I32, I32, P(I32),
@@ -242,8 +246,7 @@ def a2t_chunk_attn(c: Cache, layer: int, stream_ids: Sequence[int], n_q: Sequenc
     _check(rc, "a2t_chunk_attn")
 
 
-def a2t_append_attn(c: Cache, layer: int, stream_ids: Sequence[int], n_rows: Sequence[int], k, v,
-                    seg, pos, unit_id, n_q: Sequence[int], q, o) -> None:
+def _append_attn(fn, name, c, layer, stream_ids, n_rows, k, v, seg, pos, unit_id, n_q, q, o):
     ids, nr, nq = _i32(stream_ids), _i32(n_rows), _i32(n_q)
     if not (ids.shape == nr.shape == nq.shape):
         raise ValueError("stream_ids, n_rows and n_q differ in length")
@@ -251,11 +254,23 @@ def a2t_append_attn(c: Cache, layer: int, stream_ids: Sequence[int], n_rows: Seq
     ps = None if pos is None else _i32(pos)
     un = None if unit_id is None else _i32(unit_id)
     dt = c.torch_dtype if not isinstance(k, (int, type(None))) else None
-    rc = _lib.a2t_append_attn(c.ptr, layer, len(ids), _p(ids, C.c_int32), _p(nr, C.c_int32),
-                              _dev(k, "k", dt), _dev(v, "v", dt), _p(sg, C.c_uint8),
-                              _p(ps, C.c_int32), _p(un, C.c_int32), _p(nq, C.c_int32),
-                              _dev(q, "q", dt), _dev(o, "o", dt))
-    _check(rc, "a2t_append_attn")
+    rc = fn(c.ptr, layer, len(ids), _p(ids, C.c_int32), _p(nr, C.c_int32), _dev(k, "k", dt),
+            _dev(v, "v", dt), _p(sg, C.c_uint8), _p(ps, C.c_int32), _p(un, C.c_int32),
+            _p(nq, C.c_int32), _dev(q, "q", dt), _dev(o, "o", dt))
+    _check(rc, name)
+
+
+def a2t_append_attn(c: Cache, layer: int, stream_ids: Sequence[int], n_rows: Sequence[int], k, v,
+                    seg, pos, unit_id, n_q: Sequence[int], q, o) -> None:
+    _append_attn(_lib.a2t_append_attn, "a2t_append_attn", c, layer, stream_ids, n_rows, k, v, seg,
+                 pos, unit_id, n_q, q, o)
+
+
+def a2t_append_attn_noalloc(c: Cache, layer: int, stream_ids: Sequence[int],
+                            n_rows: Sequence[int], k, v, seg, pos, unit_id, n_q: Sequence[int],
+                            q, o) -> None:
+    _append_attn(_lib.a2t_append_attn_noalloc, "a2t_append_attn_noalloc", c, layer, stream_ids,
+                 n_rows, k, v, seg, pos, unit_id, n_q, q, o)
 
 
 def a2t_decode_attn(c: Cache, layer: int, stream_ids: Sequence[int], q, o) -> None:

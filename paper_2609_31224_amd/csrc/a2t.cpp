@@ -125,9 +125,12 @@ struct a2t_cache {
     // per-call scratch, sized at creation (no allocation on the hot path)
     std::vector<uint32_t> seen;      // stream id -> call stamp
     uint32_t stamp = 0;
-    std::vector<int32_t> tmp_nq, tmp_row0, tmp_in0;
+    std::vector<int32_t> tmp_nq, tmp_row0, tmp_in0, tmp_extra;
     std::vector<EvictPlan> evict_plans;
     bool own_pools = true;           // false: the K/V pools belong to the caller
+    // the library's fixed split workspace on this cache's device (a2t_append_attn_noalloc)
+    float* static_ws = nullptr;
+    int64_t static_ws_floats = 0;
     // attention tuning
     int target_wgs = 1024;
     int force_splits = 0;
@@ -371,12 +374,40 @@ void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_pe
     c->plan_splits.assign(splits, splits + n);
 }
 
+// Where a launch's split partials go: the cache's workspace (default) or the
+// library's fixed device array (the no-allocation entry point, which plans
+// without the workspace limit and never times its launches).
+struct WsChoice {
+    float* ws;
+    int64_t floats;
+};
+
+// Floats of split partials one launch over these streams writes at the
+// planner's choice (ws_limit as in plan_splits); `extra` rows are added to each
+// stream's resident count (a step that is about to be appended).
+int64_t planned_partials(a2t_cache* c, int n, const int32_t* ids, const int32_t* n_q,
+                         const int32_t* extra, int64_t ws_limit) {
+    const int G = c->cfg.n_q_heads / c->cfg.n_kv_heads;
+    int tiles[kMaxDesc], nsplit[kMaxDesc];
+    int64_t floats[kMaxDesc];
+    for (int i = 0; i < n; ++i) {
+        const int64_t R = c->ss[ids[i]].resident() + (extra ? extra[i] : 0);
+        tiles[i] = (int)std::max<int64_t>(1, (R + kTileKeys - 1) / kTileKeys);
+        floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
+    }
+    plan_splits(c, n, tiles, floats, nsplit, ws_limit);
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i)
+        if (nsplit[i] > 1) total += nsplit[i] * floats[i];
+    return total;
+}
+
 // One attention launch (plus merge) over up to kMaxDesc streams.
 // With in_row0 non-null (bf16 MFMA path only) the launch also appends each
 // stream's open-step rows of `layer` from k_in / v_in.
 int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_t* n_q,
                 const int32_t* q_row0, const void* q, void* o, const int32_t* in_row0 = nullptr, const void* k_in = nullptr,
-                const void* v_in = nullptr) {
+                const void* v_in = nullptr, const WsChoice* wsc = nullptr) {
     AttnBatch b{};
     b.count = n;
     b.layer = layer;
@@ -389,7 +420,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         max_rows = std::max(max_rows, n_q[i]);
         floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
     }
-    plan_splits(c, n, tiles, floats, nsplit, c->dev.ws_floats);
+    plan_splits(c, n, tiles, floats, nsplit, wsc ? INT64_MAX : c->dev.ws_floats);
     // descriptors in order of falling tiles per split: the dispatcher starts the
     // longest workgroups first
     int ord[kMaxDesc];
@@ -427,6 +458,18 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     // tile pipeline keeps more bytes in flight than the VALU kernel.
     const bool valu = c->cfg.dtype == A2T_F32 || c->force_valu;
     hipError_t e;
+    if (wsc) {
+        // the caller checked the partials against the fixed array before any state changed
+        if (off > wsc->floats) return A2T_ERR_CAPACITY;
+        DevState st = c->dev;
+        st.ws = wsc->ws;
+        st.ws_floats = wsc->floats;
+        const KTimer none{};
+        e = valu ? launch_attn_valu(st, b, q, o, c->stream, none)
+                 : launch_attn_tile(st, b, q, o, k_in, v_in, c->stream, none);
+        if (e == hipSuccess && splits > 1) e = launch_attn_merge(st, b, o, c->stream, none);
+        return e == hipSuccess ? A2T_OK : hip_fail(c);
+    }
     {
         ProfScope ps(c, valu ? "attn_valu" : "attn_tile");
         e = valu ? launch_attn_valu(c->dev, b, q, o, c->stream, ps.kt())
@@ -441,7 +484,8 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
 }
 
 int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
-                const int32_t* n_q, const void* q, void* o, bool decode) {
+                const int32_t* n_q, const void* q, void* o, bool decode,
+                const WsChoice* wsc = nullptr) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
     if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
@@ -464,7 +508,8 @@ int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* i
     DeviceGuard dg(c->cfg.device);
     for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
         const int n = std::min(kMaxDesc, n_streams - i0);
-        rc = attn_launch(c, layer, n, ids + i0, nq.data() + i0, row0.data() + i0, q, o);
+        rc = attn_launch(c, layer, n, ids + i0, nq.data() + i0, row0.data() + i0, q, o, nullptr,
+                         nullptr, nullptr, wsc);
         if (rc) return rc;
     }
     return A2T_OK;
@@ -547,6 +592,7 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     c->tmp_nq.assign(k.n_streams, 0);
     c->tmp_row0.assign(k.n_streams, 0);
     c->tmp_in0.assign(k.n_streams, 0);
+    c->tmp_extra.assign(k.n_streams, 0);
     c->evict_plans.assign(k.n_streams, EvictPlan{});
     {
         // one workgroup of the attention kernel per CU: a launch runs in rounds of CU count
@@ -596,8 +642,10 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     const int64_t lsh = (int64_t)k.n_layers * k.n_streams * k.n_kv_heads * k.head_dim * elt;
     const int64_t S = k.n_streams;
     const int64_t tot = (int64_t)k.unit_rows + k.kept_rows;
-    // workspace: enough for full splitting of one launch of every stream's max step
-    int64_t ws = (int64_t)env_int("A2T_WS_MB", 256) << 20;
+    // workspace for key-split partials (none with A2T_FLAG_NO_WORKSPACE: such a
+    // cache splits only through a2t_append_attn_noalloc and the library's fixed array)
+    const bool no_ws = (k.flags & A2T_FLAG_NO_WORKSPACE) != 0;
+    int64_t ws = no_ws ? 0 : (int64_t)env_int("A2T_WS_MB", 256) << 20;
     bool ok = true;
     auto alloc = [&](void** p, int64_t bytes) {
         if (!ok) return;
@@ -625,8 +673,13 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     alloc((void**)&d.rope, S * k.max_step_rows * (k.head_dim / 2) * 8);
     alloc((void**)&d.ev_mask, S * tot);
     alloc((void**)&d.ev_slot, S * tot * 4);
-    alloc((void**)&d.ws, ws);
+    if (!no_ws) alloc((void**)&d.ws, ws);
     d.ws_floats = ws / 4;
+    if (ok && static_scratch(k.device, &c->static_ws, &c->static_ws_floats) != hipSuccess) {
+        c->static_ws = nullptr;   // the no-allocation entry point reports NODEV
+        c->static_ws_floats = 0;
+        (void)hipGetLastError();
+    }
     // staging: per slot, seg (u8) + pos (i32) for every stream's max step, + unit ids
     c->n_slots = 16;
     c->slot_bytes = (size_t)S * k.max_step_rows * 5 + (size_t)kMaxDesc * 4 * ((S + kMaxDesc - 1) / kMaxDesc) + 256;
@@ -842,22 +895,18 @@ int a2t_chunk_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t
     return attn_common(c, layer, n_streams, ids, n_q, q, o, false);
 }
 
-int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
-                    const int32_t* n_rows, const void* kin, const void* vin, const uint8_t* seg,
-                    const int32_t* pos, const int32_t* unit_id, const int32_t* n_q,
-                    const void* q, void* o) {
-    if (!c) return A2T_ERR_INVALID;
-    if (c->poisoned) return A2T_ERR_HIP;
-    if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
-    if (!n_rows || !n_q || !q || !o || n_streams < 1 || n_streams > c->cfg.n_streams)
-        return A2T_ERR_INVALID;
-    for (int i = 0; i < n_streams; ++i)
-        if (n_q[i] < 1 || n_q[i] > n_rows[i]) return A2T_ERR_INVALID;
-    if (c->host_only) return A2T_ERR_NODEV;
+}  // extern "C"
+
+namespace {
+
+int append_attn_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                     const int32_t* n_rows, const void* kin, const void* vin, const uint8_t* seg,
+                     const int32_t* pos, const int32_t* unit_id, const int32_t* n_q, const void* q,
+                     void* o, const WsChoice* wsc) {
     const bool fused = c->cfg.dtype == A2T_BF16 && !c->force_valu;
     int rc = append_impl(c, layer, n_streams, ids, n_rows, kin, vin, seg, pos, unit_id, !fused);
     if (rc) return rc;
-    if (!fused) return attn_common(c, layer, n_streams, ids, n_q, q, o, false);
+    if (!fused) return attn_common(c, layer, n_streams, ids, n_q, q, o, false, wsc);
     DeviceGuard dg(c->cfg.device);
     std::vector<int32_t>& row0 = c->tmp_row0;
     std::vector<int32_t>& in0 = c->tmp_in0;
@@ -871,10 +920,60 @@ int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_
     for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
         const int n = std::min(kMaxDesc, n_streams - i0);
         rc = attn_launch(c, layer, n, ids + i0, n_q + i0, row0.data() + i0, q, o, in0.data() + i0,
-                         kin, vin);
+                         kin, vin, wsc);
         if (rc) return rc;
     }
     return A2T_OK;
+}
+
+int append_attn_args(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* n_rows,
+                     const int32_t* n_q, const void* q, const void* o) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
+    if (!n_rows || !n_q || !q || !o || n_streams < 1 || n_streams > c->cfg.n_streams)
+        return A2T_ERR_INVALID;
+    for (int i = 0; i < n_streams; ++i)
+        if (n_q[i] < 1 || n_q[i] > n_rows[i]) return A2T_ERR_INVALID;
+    if (c->host_only) return A2T_ERR_NODEV;
+    return A2T_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                    const int32_t* n_rows, const void* kin, const void* vin, const uint8_t* seg,
+                    const int32_t* pos, const int32_t* unit_id, const int32_t* n_q,
+                    const void* q, void* o) {
+    int rc = append_attn_args(c, layer, n_streams, n_rows, n_q, q, o);
+    if (rc) return rc;
+    return append_attn_impl(c, layer, n_streams, ids, n_rows, kin, vin, seg, pos, unit_id, n_q, q,
+                            o, nullptr);
+}
+
+int a2t_append_attn_noalloc(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,
+                            const int32_t* n_rows, const void* kin, const void* vin,
+                            const uint8_t* seg, const int32_t* pos, const int32_t* unit_id,
+                            const int32_t* n_q, const void* q, void* o) {
+    int rc = append_attn_args(c, layer, n_streams, n_rows, n_q, q, o);
+    if (rc) return rc;
+    if (!c->static_ws) return A2T_ERR_NODEV;
+    if ((rc = check_streams(c, n_streams, ids))) return rc;
+    // every launch's split partials must fit the fixed array: checked before the
+    // append changes any state (layer 0 opens the step: its rows join R)
+    std::vector<int32_t>& extra = c->tmp_extra;
+    for (int i = 0; i < n_streams; ++i) extra[i] = layer == 0 ? n_rows[i] : 0;
+    for (int i0 = 0; i0 < n_streams; i0 += kMaxDesc) {
+        const int n = std::min(kMaxDesc, n_streams - i0);
+        if (planned_partials(c, n, ids + i0, n_q + i0, extra.data() + i0, INT64_MAX) >
+            c->static_ws_floats)
+            return A2T_ERR_CAPACITY;
+    }
+    const WsChoice wsc{c->static_ws, c->static_ws_floats};
+    return append_attn_impl(c, layer, n_streams, ids, n_rows, kin, vin, seg, pos, unit_id, n_q, q,
+                            o, &wsc);
 }
 
 int a2t_decode_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* ids,

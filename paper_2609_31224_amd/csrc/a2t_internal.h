@@ -167,4 +167,9 @@ hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o,
 hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream,
                         const KTimer& kt);
 
+// The library's fixed split workspace (a file-scope device array of kernels.hip)
+// on `device`, which must be the current device: its device address and size
+// in floats.  The address is looked up once per device and kept.
+hipError_t static_scratch(int device, float** ptr, int64_t* floats);
+
 }  // namespace a2t

@@ -24,6 +24,7 @@
 #include <hip/hip_ext.h>
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 namespace a2t {
@@ -1083,7 +1084,35 @@ __global__ __launch_bounds__(256) void evict_kernel(DevState st, BT b) {
     }
 }
 
+// ------------------------------------------------------------- fixed workspace
+// Key-split partials of a2t_append_attn_noalloc: one launch's partials (every
+// split's unnormalised O rows, then their (max, sum) pairs) in a fixed device
+// array instead of a cache's workspace.  16 MiB holds the partials of a
+// 22-split launch over 22 query rows x 32 heads x head dim 128 twice over.
+// Every call on a device shares that device's copy; each attention launch
+// writes every partial its merge reads, so nothing needs clearing between calls.
+constexpr int64_t kScratchFloats = int64_t(4) << 20;
+static __device__ __align__(256) float scratch[kScratchFloats];
+constexpr int kScratchDevices = 64;
+
 }  // namespace
+
+hipError_t static_scratch(int device, float** ptr, int64_t* floats) {
+    static std::mutex mu;
+    static float* addr[kScratchDevices] = {};
+    if (device < 0 || device >= kScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[device]) {
+        // the array's name is a host-side stand-in: kernels get this device address
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[device] = static_cast<float*>(p);
+    }
+    *ptr = addr[device];
+    *floats = kScratchFloats;
+    return hipSuccess;
+}
 
 // ------------------------------------------------------------------ launchers
 // One dispatch, through hipExtLaunchKernelGGL when the caller asks for timestamps.
