@@ -95,6 +95,8 @@ METRICS = {
     "distill": ("objective evaluations/s (masked CE + T^2 KL + group-balanced means and the "
                 "student-logit gradient over a 16-utterance batch)", "evaluations/s"),
     "copy": ("device copy bandwidth (read + write bytes per second)", "GB/s"),
+    "graph": ("stream unit-steps/s (append+attn+evict), device-planned steps, one HIP graph "
+              "replay per unit", "unit-steps/s"),
 }
 DEFAULTS = {  # warmup, steps, profile steps
     "stream": (3, 397, 0),
@@ -105,6 +107,7 @@ DEFAULTS = {  # warmup, steps, profile steps
     "distill": (5, 40, 20),
     "hour": (0, 100, 20),
     "copy": (3, 20, 0),
+    "graph": (5, 20, 0),
 }
 
 
@@ -552,6 +555,113 @@ def run_stream(args):
         "cpu_baseline": base_line,
     }
     return res
+
+# ------------------------------------------------------- device-planned graph replay
+def run_graph(args):
+    """The ten-minute stream through the device-planned calls (a2t_dev_*): the
+    device opens each unit from metadata in device memory, plans its key splits
+    and the eviction.  Eight HIP graphs (one per slot of the pre-generated
+    value pool) each hold a whole unit: a cursor copies the next unit's row
+    metadata from a device-resident table into the step's buffers and advances
+    itself, then the open, the 36 layers' append + attention and the eviction.
+    The host replays one graph per unit.  The same 600-unit session runs
+    twice, once replaying the graphs and once issuing the same calls eagerly;
+    units FILL_UNITS + --warmup onward are timed for --steps units in each."""
+    import torch
+    import paper_2609_31224_amd as a2t
+    cfg = CONFIGS[1]
+    first = FILL_UNITS + args.warmup
+    if args.warmup < 0 or args.steps < 1 or first + args.steps > SESSION_UNITS:
+        raise SystemExit(f"--warmup + --steps <= {SESSION_UNITS - FILL_UNITS}")
+    last = first + args.steps
+    spec = make_workload(cfg, seed=args.seed).streams[0]
+    L, Hq, Hkv, D, MS = cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.max_unit_rows
+    keep_rows = sum(int(np.isin(st.seg, KEEP_SEGS).sum()) for st in spec.steps)
+    unit_rows = max(cfg.budget, cfg.window * MS) + 2 * MS
+    n_units = len(spec.steps)
+    meta = np.zeros((n_units, 2 + MS), np.int32)   # n_rows, unit id, positions
+    segs = np.zeros((n_units, MS), np.uint8)
+    for u, st in enumerate(spec.steps):
+        meta[u, 0], meta[u, 1] = st.n, st.unit
+        meta[u, 2:2 + st.n] = st.pos
+        segs[u, :st.n] = st.seg
+    side = torch.cuda.Stream()
+
+    def session(replay):
+        with torch.cuda.stream(side):
+            r = Runner(cfg, 1, unit_rows, keep_rows + 64, MS)
+            dev = r.dev
+            qp = r.pool((POOL, L, MS, Hq, D), args.seed)
+            kp = r.pool((POOL, L, MS, Hkv, D), args.seed + 1)
+            vp = r.pool((POOL, L, MS, Hkv, D), args.seed + 2)
+            out = torch.empty(L, MS, Hq, D, dtype=torch.bfloat16, device=dev)
+            table = torch.from_numpy(meta).to(dev)
+            seg_table = torch.from_numpy(segs).to(dev)
+            cur = torch.zeros(2 + MS, dtype=torch.int32, device=dev)
+            cur_seg = torch.zeros(MS, dtype=torch.uint8, device=dev)
+            cursor = torch.zeros(1, dtype=torch.int64, device=dev)
+            budget = torch.tensor([cfg.budget], dtype=torch.int32, device=dev)
+            c = r.cache
+
+            def unit_calls(p):
+                cur.copy_(table.index_select(0, cursor).view(-1))
+                cur_seg.copy_(seg_table.index_select(0, cursor).view(-1))
+                cursor.add_(1)
+                a2t.a2t_dev_open(c, [0], cur[0:1], cur[1:2], cur_seg, cur[2:])
+                for layer in range(L):
+                    a2t.a2t_dev_append_attn(c, layer, kp[p, layer], vp[p, layer], qp[p, layer],
+                                            out[layer])
+                a2t.a2t_dev_evict(c, budget, cfg.window)
+
+            a2t.a2t_dev_begin(c)
+            graphs = []
+            if replay:
+                for p in range(POOL):
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=side):
+                        unit_calls(p)
+                    graphs.append(g)
+                cursor.zero_()
+            run_unit = (lambda u: graphs[u % POOL].replay()) if replay else \
+                (lambda u: unit_calls(u % POOL))
+            for u in range(first):
+                run_unit(u)
+            step_ms, total_ms, t_wall, t_enq = r.timed(lambda j: run_unit(first + j), args.steps)
+            for u in range(last, SESSION_UNITS):
+                run_unit(u)
+            a2t.a2t_dev_end(c)
+            info = r.stream_info(0)
+            res = {"step_ms": step_ms, "total_ms": total_ms, "t_wall": t_wall, "t_enq": t_enq,
+                   "peak": info.peak, "end": info.resident}
+            r.close()
+            return res
+
+    graph = session(True)
+    eager = session(False)
+    ms_per_step = graph["total_ms"] / args.steps
+    return {
+        "value": 1000.0 / ms_per_step,
+        "ms_per_step": ms_per_step,
+        "config": {
+            "workload": "ten-minute single stream: 36 layers, 32 query / 8 KV heads, head dim 128, "
+                        "bf16, units of 17 acoustic + 2 delimiter + Poisson(3) transcript rows, "
+                        "budget 4096 rows, recent window 30 units",
+            "session_units": SESSION_UNITS, "fill_units": FILL_UNITS, "timed_units": [first, last],
+            "calls": "per unit one HIP graph replay: metadata cursor (3 small copy/add kernels), "
+                     "a2t_dev_open, a2t_dev_append_attn x 36, a2t_dev_evict",
+            "seed": args.seed,
+        },
+        **timing_fields(graph["step_ms"], graph["total_ms"], args.steps, graph["t_wall"],
+                        graph["t_enq"]),
+        "eager_device_planned": {"value": 1000.0 * args.steps / eager["total_ms"],
+                                 "ms_per_step": eager["total_ms"] / args.steps,
+                                 "host_enqueue_ms_per_step": eager["t_enq"] * 1e3 / args.steps},
+        "peak_rows": graph["peak"], "end_rows": graph["end"],
+        "same_session_end": graph["end"] == eager["end"] and graph["peak"] == eager["peak"],
+        "roofline": None,
+        "cpu_baseline": None,
+    }
+
 
 # ------------------------------------------------------------------- varlen batch
 def _varlen_session(args, kernel):
@@ -1011,7 +1121,13 @@ def run_sweep(args):
     rows = []
     value = None
     last = None
-    for B in (None, 8000, 6000, 4000, 0):
+    # the paper's rule over Table 3's budgets, then its two variants: per-row
+    # granularity at the selected budget, and the StreamingLLM comparison (4
+    # sink rows + 2,000 recent positions, Table 1)
+    sweep = [(B, None, 0) for B in (None, 8000, 6000, 4000, 0)] + \
+        [(4000, "row", 0), (4 + 2000, "sink_recent", 4)]
+    rule_ids = {None: 0, "row": 1, "sink_recent": 2}
+    for B, rule, n_sink in sweep:
         r = Runner(cfg, S, total + 64, keep_rows + 64, max_n)
         torch, lib, h = r.torch, r.lib, r.h
         if last is None:
@@ -1035,18 +1151,26 @@ def run_sweep(args):
                 r.check(lib.a2t_append_attn(h, layer, S, ids, nrows, kp.data_ptr() + okv,
                                             vp.data_ptr() + okv, *meta, nrows, qp.data_ptr() + oq,
                                             out.data_ptr()), "a2t_append_attn")
-            if B is not None:
+            if B is not None and rule is None:
                 r.check(lib.a2t_evict(h, S, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
+            elif B is not None:
+                r.check(lib.a2t_evict_rule(h, S, ids, budget, cfg.window, rule_ids[rule], n_sink,
+                                           n_ev, unmet), "a2t_evict_rule")
 
         step_ms, total_ms, t_wall, t_enq = r.timed(run_unit, n_units)
         ends = [r.stream_info(i).resident for i in range(S)]
         peaks = [r.stream_info(i).peak for i in range(S)]
         r.close()
-        rows.append({"budget": "unbounded" if B is None else B, "end_rows_mean": float(np.mean(ends)),
+        if rule == "sink_recent":
+            label = f"{n_sink} sinks + {B - n_sink} recent (StreamingLLM)"
+        else:
+            label = "per-row (ablation)" if rule == "row" else "unit (Sec. 3.3)"
+        rows.append({"budget": "unbounded" if B is None else B, "rule": label,
+                     "end_rows_mean": float(np.mean(ends)),
                      "peak_rows_mean": float(np.mean(peaks)), "step_ms_mean": float(step_ms.mean()),
                      "step_ms_p99": float(np.percentile(step_ms, 99)),
                      "steps_over_1s": int((step_ms > 1000).sum())})
-        if B == 4000:
+        if B == 4000 and rule is None:
             value = S * n_units / (total_ms * 1e-3)
             ms_per_step = total_ms / n_units
     return {
@@ -1055,10 +1179,12 @@ def run_sweep(args):
         "config": {
             "workload": "budget sweep: 15 synthetic ten-minute sessions (600 units of 17 acoustic + "
                         "2 delimiter + Poisson(3) transcript rows) batched in one cache; budgets "
-                        "unbounded/8000/6000/4000/0 rows, recent window 30 units; 36 layers, 32 "
+                        "unbounded/8000/6000/4000/0 rows, recent window 30 units, then per-row "
+                        "eviction at 4000 and 4 sinks + 2000 recent rows; 36 layers, 32 "
                         "query / 8 KV heads, head dim 128, bf16",
             "sessions": S, "units": n_units,
-            "calls": "a2t_append_attn per layer over all sessions, one a2t_evict per unit",
+            "calls": "a2t_append_attn per layer over all sessions, one a2t_evict (or "
+                     "a2t_evict_rule) per unit",
             "seed": args.seed,
         },
         "sweep": rows,
@@ -1236,11 +1362,11 @@ def main():
     args.profile_steps = p if args.profile_steps is None else args.profile_steps
     if args.seed is None:
         args.seed = {"stream": 1, "varlen": 2, "decode": 3, "cadence": 1, "sweep": 1,
-                     "distill": 14, "hour": 4, "copy": 0}[args.workload]
+                     "distill": 14, "hour": 4, "copy": 0, "graph": 1}[args.workload]
 
     res = {"stream": run_stream, "varlen": run_varlen, "decode": run_decode,
            "cadence": run_cadence, "sweep": run_sweep, "distill": run_distill,
-           "hour": run_hour, "copy": run_copy}[args.workload](args)
+           "hour": run_hour, "copy": run_copy, "graph": run_graph}[args.workload](args)
     metric, unit = METRICS[args.workload]
     result = {
         "metric": metric,

@@ -295,6 +295,68 @@ int a2t_evict_rule(a2t_cache* c, int32_t n_streams, const int32_t* stream_ids,
                    const int32_t* budget, int32_t window, int32_t rule, int32_t n_sink,
                    int32_t* n_evicted, uint8_t* budget_unmet);
 
+/* ---------------------------------------------------------------------------
+ * Device-planned steps: the same listening or decode step (append + chunk
+ * attention on every layer, then Sec. 3.3's eviction check) with every
+ * per-step decision taken on the device, from step metadata the caller leaves
+ * in device memory.  Each call below enqueues kernels whose arguments do not
+ * depend on the step, so a caller can capture a whole step (or one layer's
+ * call among its own kernels) in a HIP graph once and replay it for every
+ * later step, rewriting only the contents of its device buffers in between.
+ *
+ * Between a2t_dev_begin and a2t_dev_end the device holds each stream's state
+ * (rows, ring head, newest unit and position, the per-unit eviction plan): the
+ * host-planned calls (a2t_append*, a2t_*_attn, a2t_evict*, a2t_stream_info_get,
+ * a2t_read_*) return A2T_ERR_STATE.  Only bf16 caches (the fused MFMA path);
+ * at most 64 streams per step; eviction follows Sec. 3.3's whole-unit rule.
+ * ------------------------------------------------------------------------- */
+
+/* Hand the host's per-stream state to the device (synchronises).  Errors:
+ * INVALID (fp32 cache), STATE (already begun, or a host step still open),
+ * NODEV (host-only cache). */
+int a2t_dev_begin(a2t_cache* c);
+
+/* Take the state back (synchronises): the host's bookkeeping then describes
+ * the cache as the device-planned steps left it.  Returns A2T_OK, or the first
+ * status a device-planned step reported for some stream (see a2t_dev_open);
+ * the cache is consistent either way.  Errors: STATE (not begun, or a step is
+ * open). */
+int a2t_dev_end(a2t_cache* c);
+
+/* Open one step for n_streams listed streams (host ids, distinct).  Device
+ * arrays, read when the stream reaches the work:
+ *   n_rows   [n_streams]  rows of each stream's step (1..max_step_rows)
+ *   unit_id  [n_streams]  as in a2t_append
+ *   seg      [n_streams][max_step_rows]  a2t_seg per row (first n_rows used)
+ *   pos      [n_streams][max_step_rows]  position ids, strictly increasing
+ * The device checks what a2t_append checks; a stream whose step fails a check
+ * records the status (returned by a2t_dev_end) and takes no part in this or
+ * any later device-planned step.  The device then plans each stream's key
+ * splits (the smallest budget of key tiles per split whose workgroups fit one
+ * round over the CUs, as the host plans a single stream).
+ * Errors (host-side, nothing enqueued): INVALID (ids, null pointers, more than
+ * 64 streams), STATE (not begun, or the previous step not evicted). */
+int a2t_dev_open(a2t_cache* c, int32_t n_streams, const int32_t* stream_ids, const int32_t* n_rows,
+                 const int32_t* unit_id, const uint8_t* seg, const int32_t* pos);
+
+/* a2t_append_attn for one layer of the open step.  k, v: device
+ * [n_streams][max_step_rows][Hkv][D]; q, o: device [n_streams][max_step_rows]
+ * [Hq][D]: listed stream i's rows start at row i * max_step_rows (only its
+ * first n_rows are read or written).  Errors: INVALID, STATE (no open step,
+ * or the layer already appended). */
+int a2t_dev_append_attn(a2t_cache* c, int32_t layer, const void* k, const void* v, const void* q,
+                        void* o);
+
+/* Sec. 3.3's eviction for the open step's streams, planned on the device:
+ * while R > budget[i], the oldest unit outside the window that still holds
+ * acoustic/structural rows loses all of them.  budget: device [n_streams]
+ * (negative counts as 0); n_evicted, budget_unmet: optional device
+ * [n_streams] outputs.  Closes the step.  Errors: INVALID, STATE (no open
+ * step, or a layer not appended).  A kept region that would overflow is
+ * reported by a2t_dev_end (CAPACITY) and that stream evicts nothing. */
+int a2t_dev_evict(a2t_cache* c, const int32_t* budget, int32_t window, int32_t* n_evicted,
+                  uint8_t* budget_unmet);
+
 /* Bookkeeping of one stream (host state, no synchronisation). */
 int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out);
 

@@ -38,7 +38,8 @@ SEG_PREFIX, SEG_ACOUSTIC, SEG_DELIM, SEG_TEXT, SEG_RESPONSE = 0, 1, 2, 3, 4
 EXPORTED = (
     "a2t_cache_create", "a2t_cache_destroy", "a2t_set_stream", "a2t_append",
     "a2t_chunk_attn", "a2t_append_attn", "a2t_append_attn_noalloc", "a2t_decode_attn",
-    "a2t_evict", "a2t_evict_rule",
+    "a2t_evict", "a2t_evict_rule", "a2t_dev_begin", "a2t_dev_end", "a2t_dev_open",
+    "a2t_dev_append_attn", "a2t_dev_evict",
     "a2t_stream_info_get",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
     "a2t_profile_enable", "a2t_kernel_time", "a2t_profile_reserve", "a2t_status_str",
@@ -95,6 +96,11 @@ def _load():
         "a2t_evict": (C.c_int, [VP, I32, P(I32), P(I32), I32, P(I32), P(C.c_uint8)]),
         "a2t_evict_rule": (C.c_int, [VP, I32, P(I32), P(I32), I32, I32, I32, P(I32),
                                      P(C.c_uint8)]),
+        "a2t_dev_begin": (C.c_int, [VP]),
+        "a2t_dev_end": (C.c_int, [VP]),
+        "a2t_dev_open": (C.c_int, [VP, I32, P(I32), VP, VP, VP, VP]),
+        "a2t_dev_append_attn": (C.c_int, [VP, I32, VP, VP, VP, VP]),
+        "a2t_dev_evict": (C.c_int, [VP, VP, I32, VP, VP]),
         "a2t_stream_info_get": (C.c_int, [VP, I32, P(a2t_stream_info)]),
         "a2t_read_layout": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
         "a2t_read_last_evict": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
@@ -302,6 +308,38 @@ def a2t_evict_rule(c: Cache, stream_ids: Sequence[int], budget, window: int, rul
                              n_sink, _p(n_ev, C.c_int32), _p(unmet, C.c_uint8))
     _check(rc, "a2t_evict_rule")
     return n_ev, unmet.astype(bool)
+
+
+def a2t_dev_begin(c: Cache) -> None:
+    _check(_lib.a2t_dev_begin(c.ptr), "a2t_dev_begin")
+
+
+def a2t_dev_end(c: Cache) -> None:
+    _check(_lib.a2t_dev_end(c.ptr), "a2t_dev_end")
+
+
+def a2t_dev_open(c: Cache, stream_ids: Sequence[int], n_rows, unit_id, seg, pos) -> None:
+    """n_rows, unit_id: device int32 [n]; seg: device uint8 [n][max_step_rows];
+    pos: device int32 [n][max_step_rows] (torch tensors or addresses)."""
+    ids = _i32(stream_ids)
+    rc = _lib.a2t_dev_open(c.ptr, len(ids), _p(ids, C.c_int32), _dev(n_rows, "n_rows"),
+                           _dev(unit_id, "unit_id"), _dev(seg, "seg"), _dev(pos, "pos"))
+    _check(rc, "a2t_dev_open")
+
+
+def a2t_dev_append_attn(c: Cache, layer: int, k, v, q, o) -> None:
+    dt = c.torch_dtype if not isinstance(k, int) else None
+    rc = _lib.a2t_dev_append_attn(c.ptr, layer, _dev(k, "k", dt), _dev(v, "v", dt),
+                                  _dev(q, "q", dt), _dev(o, "o", dt))
+    _check(rc, "a2t_dev_append_attn")
+
+
+def a2t_dev_evict(c: Cache, budget, window: int, n_evicted=None, budget_unmet=None) -> None:
+    """budget: device int32 [n]; n_evicted (int32), budget_unmet (uint8): optional
+    device [n] outputs."""
+    rc = _lib.a2t_dev_evict(c.ptr, _dev(budget, "budget"), window, _dev(n_evicted, "n_evicted"),
+                            _dev(budget_unmet, "budget_unmet"))
+    _check(rc, "a2t_dev_evict")
 
 
 def a2t_stream_info_get(c: Cache, stream: int) -> dict:

@@ -131,6 +131,18 @@ struct a2t_cache {
     // the library's fixed split workspace on this cache's device (a2t_append_attn_noalloc)
     float* static_ws = nullptr;
     int64_t static_ws_floats = 0;
+    // device-planned steps (a2t_dev_*): the plan the device writes, the call
+    // sequence the host checks, a host copy of the device's per-stream state
+    DevPlan* dplan = nullptr;
+    bool dev_mode = false;
+    bool dev_step_open = false;
+    int dev_count = 0;
+    int dev_max_splits = 1;
+    int32_t dev_ids[kMaxDesc] = {};
+    std::vector<uint8_t> dev_layers;
+    std::vector<DevStream> dss_host;
+    std::vector<int32_t> uid_host;
+    std::vector<uint8_t> seg_host;
     // attention tuning
     int target_wgs = 1024;
     int force_splits = 0;
@@ -488,6 +500,7 @@ int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* i
                 const WsChoice* wsc = nullptr) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
+    if (c->dev_mode) return A2T_ERR_STATE;
     if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
     int rc = check_streams(c, n_streams, ids);
     if (rc) return rc;
@@ -523,7 +536,7 @@ void free_device(a2t_cache* c) {
     }
     void* ptrs[] = {c->dev.unit_pos, c->dev.unit_uid, c->dev.unit_seg, c->dev.kept_pos,
                     c->dev.kept_uid, c->dev.kept_seg, c->dev.rope, c->dev.ev_mask,
-                    c->dev.ev_slot, c->dev.ws};
+                    c->dev.ev_slot, c->dev.ws, c->dev.dss, c->dplan};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     if (c->stage) (void)hipHostFree(c->stage);
@@ -675,6 +688,8 @@ int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out) {
     alloc((void**)&d.ev_slot, S * tot * 4);
     if (!no_ws) alloc((void**)&d.ws, ws);
     d.ws_floats = ws / 4;
+    alloc((void**)&d.dss, S * (int64_t)sizeof(DevStream));
+    alloc((void**)&c->dplan, (int64_t)sizeof(DevPlan));
     if (ok && static_scratch(k.device, &c->static_ws, &c->static_ws_floats) != hipSuccess) {
         c->static_ws = nullptr;   // the no-allocation entry point reports NODEV
         c->static_ws_floats = 0;
@@ -729,6 +744,7 @@ static int append_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int
                        bool launch_rows) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
+    if (c->dev_mode) return A2T_ERR_STATE;
     const a2t_config& k = c->cfg;
     if (layer < A2T_ALL_LAYERS || layer >= k.n_layers) return A2T_ERR_INVALID;
     int rc = check_streams(c, n_streams, ids);
@@ -930,6 +946,7 @@ int append_attn_args(a2t_cache* c, int32_t layer, int32_t n_streams, const int32
                      const int32_t* n_q, const void* q, const void* o) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
+    if (c->dev_mode) return A2T_ERR_STATE;
     if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
     if (!n_rows || !n_q || !q || !o || n_streams < 1 || n_streams > c->cfg.n_streams)
         return A2T_ERR_INVALID;
@@ -1096,6 +1113,7 @@ int evict_impl(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_
                uint8_t* budget_unmet) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
+    if (c->dev_mode) return A2T_ERR_STATE;
     int rc = check_streams(c, n_streams, ids);
     if (rc) return rc;
     if (!budget || window < 0) return A2T_ERR_INVALID;
@@ -1179,6 +1197,7 @@ int a2t_evict_rule(a2t_cache* c, int32_t n_streams, const int32_t* ids, const in
 
 int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out) {
     if (!c || !out || stream < 0 || stream >= c->cfg.n_streams) return A2T_ERR_INVALID;
+    if (c->dev_mode) return A2T_ERR_STATE;   // the device holds the state (a2t_dev_end)
     const StreamState& s = c->ss[stream];
     out->resident = s.resident();
     out->peak = s.peak;
@@ -1209,6 +1228,7 @@ int a2t_sync(a2t_cache* c) {
 int a2t_read_layout(a2t_cache* c, int32_t stream, int32_t* pos, uint8_t* seg, int32_t* unit) {
     if (!c || stream < 0 || stream >= c->cfg.n_streams) return A2T_ERR_INVALID;
     if (c->host_only) return A2T_ERR_NODEV;
+    if (c->dev_mode) return A2T_ERR_STATE;
     int rc = a2t_sync(c);
     if (rc) return rc;
     DeviceGuard dg(c->cfg.device);
@@ -1236,6 +1256,7 @@ int a2t_read_last_evict(a2t_cache* c, int32_t stream, int32_t* n_pre, uint8_t* m
                         int32_t* new_slot) {
     if (!c || stream < 0 || stream >= c->cfg.n_streams) return A2T_ERR_INVALID;
     if (c->host_only) return A2T_ERR_NODEV;
+    if (c->dev_mode) return A2T_ERR_STATE;
     const StreamState& s = c->ss[stream];
     if (s.last_evict_pre < 0) return A2T_ERR_STATE;
     int rc = a2t_sync(c);
@@ -1254,6 +1275,7 @@ int a2t_read_kv(a2t_cache* c, int32_t layer, int32_t stream, void* kout, void* v
     if (!c || stream < 0 || stream >= c->cfg.n_streams || layer < 0 || layer >= c->cfg.n_layers)
         return A2T_ERR_INVALID;
     if (c->host_only) return A2T_ERR_NODEV;
+    if (c->dev_mode) return A2T_ERR_STATE;
     int rc = a2t_sync(c);
     if (rc) return rc;
     DeviceGuard dg(c->cfg.device);
@@ -1326,6 +1348,154 @@ int a2t_kernel_time(a2t_cache* c, const char* kernel, int64_t* launches, double*
     }
     if (launches) *launches = n;
     if (total_ms) *total_ms = ms;
+    return A2T_OK;
+}
+
+// ---- device-planned steps --------------------------------------------------------
+int a2t_dev_begin(a2t_cache* c) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (c->host_only) return A2T_ERR_NODEV;
+    if (c->cfg.dtype != A2T_BF16 || c->force_valu) return A2T_ERR_INVALID;
+    if (c->dev_mode) return A2T_ERR_STATE;
+    for (const StreamState& s : c->ss)
+        if (!s.step_complete() || s.step_rows != 0) return A2T_ERR_STATE;
+    c->dss_host.resize(c->cfg.n_streams);
+    for (int i = 0; i < c->cfg.n_streams; ++i) {
+        const StreamState& s = c->ss[i];
+        DevStream& d = c->dss_host[i];
+        d = DevStream{};
+        d.kept = s.kept;
+        d.head = s.head;
+        d.ring = s.ring;
+        d.cur_unit = s.cur_unit;
+        d.last_pos = s.last_pos;
+        d.peak = s.peak;
+        d.last_evicted = s.last_evicted;
+        d.evicted_total = s.evicted_total;
+        d.moved_total = s.moved_total;
+        d.budget_unmet = s.budget_unmet;
+        d.last_evict_pre = s.last_evict_pre;
+    }
+    DeviceGuard dg(c->cfg.device);
+    if (hipStreamSynchronize(c->stream) != hipSuccess ||
+        hipMemcpy(c->dev.dss, c->dss_host.data(), sizeof(DevStream) * c->dss_host.size(),
+                  hipMemcpyHostToDevice) != hipSuccess)
+        return hip_fail(c);
+    c->dev_mode = true;
+    c->dev_step_open = false;
+    c->dev_layers.assign(c->cfg.n_layers, 0);
+    return A2T_OK;
+}
+
+int a2t_dev_end(a2t_cache* c) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (!c->dev_mode || c->dev_step_open) return A2T_ERR_STATE;
+    DeviceGuard dg(c->cfg.device);
+    const int S = c->cfg.n_streams, cap = c->cfg.unit_rows;
+    c->uid_host.resize((size_t)S * cap);
+    c->seg_host.resize((size_t)S * cap);
+    if (hipStreamSynchronize(c->stream) != hipSuccess ||
+        hipMemcpy(c->dss_host.data(), c->dev.dss, sizeof(DevStream) * S, hipMemcpyDeviceToHost) != hipSuccess ||
+        hipMemcpy(c->uid_host.data(), c->dev.unit_uid, (size_t)S * cap * 4, hipMemcpyDeviceToHost) != hipSuccess ||
+        hipMemcpy(c->seg_host.data(), c->dev.unit_seg, (size_t)S * cap, hipMemcpyDeviceToHost) != hipSuccess)
+        return hip_fail(c);
+    int err = A2T_OK;
+    for (int i = 0; i < S; ++i) {
+        const DevStream& d = c->dss_host[i];
+        StreamState& s = c->ss[i];
+        if (d.error && err == A2T_OK) err = d.error;
+        s.kept = d.kept;
+        s.head = d.head;
+        s.ring = d.ring;
+        s.cur_unit = d.cur_unit;
+        s.last_pos = d.last_pos;
+        s.peak = d.peak;
+        s.last_evicted = d.last_evicted;
+        s.evicted_total = d.evicted_total;
+        s.moved_total = d.moved_total;
+        s.budget_unmet = d.budget_unmet;
+        s.last_evict_pre = d.last_evict_pre;
+        s.step_rows = 0;
+        std::fill(s.appended.begin(), s.appended.end(), 1);
+        // the unit queue and class ring from the ring slots' metadata
+        s.units.pop_front(s.units.size());
+        for (int x = 0; x < s.ring; ++x) {
+            const int slot = (s.head + x) % cap;
+            const int32_t u = c->uid_host[(size_t)i * cap + slot];
+            const uint8_t sg = c->seg_host[(size_t)i * cap + slot];
+            s.ring_seg[slot] = sg;
+            if (s.units.size() && s.units.back().unit == u) {
+                s.units.back().rows += 1;
+                s.units.back().evictable += is_evictable(sg);
+            } else {
+                s.units.push_back(UnitRec{u, 1, is_evictable(sg) ? 1 : 0});
+            }
+        }
+    }
+    c->dev_mode = false;
+    return err;
+}
+
+int a2t_dev_open(a2t_cache* c, int32_t n_streams, const int32_t* ids, const int32_t* n_rows,
+                 const int32_t* unit_id, const uint8_t* seg, const int32_t* pos) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (!c->dev_mode || c->dev_step_open) return A2T_ERR_STATE;
+    if (n_streams > kMaxDesc || !n_rows || !unit_id || !seg || !pos) return A2T_ERR_INVALID;
+    int rc = check_streams(c, n_streams, ids);
+    if (rc) return rc;
+    DevStepArgs a{};
+    a.count = n_streams;
+    a.target_wgs = c->target_wgs;
+    a.max_splits = std::max(1, std::min(kMaxSplits, c->target_wgs / c->cfg.n_kv_heads));
+    for (int i = 0; i < n_streams; ++i) a.ids[i] = ids[i];
+    DeviceGuard dg(c->cfg.device);
+    if (launch_dev_open(c->dev, a, n_rows, unit_id, seg, pos, c->dplan, c->stream) != hipSuccess ||
+        launch_step_meta_dev(c->dev, c->dplan, n_streams, seg, pos, unit_id, c->stream) != hipSuccess)
+        return hip_fail(c);
+    c->dev_step_open = true;
+    c->dev_count = n_streams;
+    c->dev_max_splits = a.max_splits;
+    std::copy(ids, ids + n_streams, c->dev_ids);
+    std::fill(c->dev_layers.begin(), c->dev_layers.end(), 0);
+    return A2T_OK;
+}
+
+int a2t_dev_append_attn(a2t_cache* c, int32_t layer, const void* k, const void* v, const void* q,
+                        void* o) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (!c->dev_mode || !c->dev_step_open) return A2T_ERR_STATE;
+    if (layer < 0 || layer >= c->cfg.n_layers || !k || !v || !q || !o) return A2T_ERR_INVALID;
+    if (c->dev_layers[layer]) return A2T_ERR_STATE;
+    DeviceGuard dg(c->cfg.device);
+    if (launch_attn_tile_dev(c->dev, c->dplan, c->dev_count, c->dev_max_splits, layer, q, o, k, v,
+                             c->stream) != hipSuccess ||
+        launch_attn_merge_dev(c->dev, c->dplan, c->dev_count, c->dev_max_splits, o, c->stream) !=
+            hipSuccess)
+        return hip_fail(c);
+    c->dev_layers[layer] = 1;
+    return A2T_OK;
+}
+
+int a2t_dev_evict(a2t_cache* c, const int32_t* budget, int32_t window, int32_t* n_evicted,
+                  uint8_t* budget_unmet) {
+    if (!c) return A2T_ERR_INVALID;
+    if (c->poisoned) return A2T_ERR_HIP;
+    if (!c->dev_mode || !c->dev_step_open) return A2T_ERR_STATE;
+    if (!budget || window < 0) return A2T_ERR_INVALID;
+    for (uint8_t l : c->dev_layers)
+        if (!l) return A2T_ERR_STATE;
+    DevStepArgs a{};
+    a.count = c->dev_count;
+    a.window = window;
+    std::copy(c->dev_ids, c->dev_ids + c->dev_count, a.ids);
+    DeviceGuard dg(c->cfg.device);
+    if (launch_dev_evict(c->dev, a, budget, n_evicted, budget_unmet, c->dplan, c->stream) != hipSuccess)
+        return hip_fail(c);
+    c->dev_step_open = false;
     return A2T_OK;
 }
 

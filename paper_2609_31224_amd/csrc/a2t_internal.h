@@ -21,6 +21,20 @@ constexpr int kMaxSplits = 128;
 // Query rows per workgroup of the split merge.
 constexpr int kMergeRows = 4;
 
+// State of one stream kept on the device for device-planned steps (the host's
+// per-stream mirror, moved to the device while the caller drives the cache
+// with a2t_dev_* calls).
+struct DevStream {
+    int32_t kept, head, ring, cur_unit;
+    int64_t last_pos;
+    int32_t step_rows, step_slot0;
+    int32_t peak, last_evicted;
+    int64_t evicted_total, moved_total;
+    int32_t budget_unmet, last_evict_pre;
+    int32_t error;      // first a2t_status a device-planned step hit on this stream (0: none)
+    int32_t pad_;
+};
+
 // Device-side buffers of a cache and its shape.
 struct DevState {
     void* k_unit;   // [L][S][Hkv][unit_rows][D]  rotated keys of the rows eviction has not
@@ -38,6 +52,7 @@ struct DevState {
     int32_t* ev_slot;   // [S][unit_rows + kept_rows] last eviction, new slot or -1
     float* ws;          // split-K attention partials
     int64_t ws_floats;
+    DevStream* dss;     // [S] device-planned steps: per-stream state
     int32_t L, S, Hq, Hkv, D, dtype;
     int32_t G;          // query heads per KV head (Hq / Hkv)
     int32_t unit_rows, kept_rows, max_step_rows;
@@ -129,6 +144,40 @@ struct EvictBatchT {
 };
 using EvictBatch = EvictBatchT<kMaxDesc>;
 
+// ---- device-planned steps: descriptors written by device kernels
+// Descriptors read through a pointer to device memory instead of from the
+// kernel arguments; `layer` and `max_rows` still come with the launch.  The
+// kernels index `b.d[i]` and read `b.layer` / `b.max_rows` the same way for
+// both kinds of batch.
+template <class Desc>
+struct DescPtr {
+    const Desc* p;
+    __device__ const Desc& operator[](int i) const { return p[i]; }
+};
+template <class Desc>
+struct DevBatch {
+    DescPtr<Desc> d;
+    int32_t layer;
+    int32_t max_rows;
+};
+
+// What a device-planned step's kernels read: written by dev_open_kernel
+// (metadata, attention) and dev_evict_plan_kernel (eviction).
+struct DevPlan {
+    StepDesc step[kMaxDesc];
+    AttnDesc attn[kMaxDesc];
+    EvictDesc evict[kMaxDesc];
+};
+
+// Kernel argument of the device planners: the streams of the step and limits.
+struct DevStepArgs {
+    int32_t count;
+    int32_t max_splits;   // key splits the attention grid was sized for
+    int32_t target_wgs;   // workgroups one attention launch spreads over at most
+    int32_t window;       // recent units protected (eviction)
+    int32_t ids[kMaxDesc];
+};
+
 // Kernel arguments are copied per launch: a launch carries a batch sized to
 // its stream count (1, 8 or kMaxDesc descriptors), not always the largest.
 template <template <int> class BT, int N>
@@ -166,6 +215,28 @@ hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o,
                              hipStream_t stream, const KTimer& kt);
 hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream,
                         const KTimer& kt);
+
+// Device-planned steps (bf16 caches: the fused MFMA path).  dev_open: validate the step's device-resident
+// metadata (n_rows, unit [count]; seg, pos [count][max_step_rows]), open it in
+// every listed stream and write the metadata, attention and step descriptors
+// to `plan`.  Then the per-layer launches read `plan` (metadata + rotary
+// table once, attention + merge per layer).  dev_evict: plan Sec. 3.3's
+// eviction on the device (budget [count], n_evicted / budget_unmet [count]
+// out, may be null) and run it.
+hipError_t launch_dev_open(const DevState& st, const DevStepArgs& a, const int32_t* n_rows,
+                           const int32_t* unit, const uint8_t* seg, const int32_t* pos,
+                           DevPlan* plan, hipStream_t stream);
+hipError_t launch_step_meta_dev(const DevState& st, const DevPlan* plan, int count,
+                                const uint8_t* seg, const int32_t* pos, const int32_t* unit,
+                                hipStream_t stream);
+hipError_t launch_attn_tile_dev(const DevState& st, const DevPlan* plan, int count,
+                                int max_splits, int layer, const void* q, void* o,
+                                const void* k_in, const void* v_in, hipStream_t stream);
+hipError_t launch_attn_merge_dev(const DevState& st, const DevPlan* plan, int count,
+                                 int max_splits, void* o, hipStream_t stream);
+hipError_t launch_dev_evict(const DevState& st, const DevStepArgs& a, const int32_t* budget,
+                            int32_t* n_evicted, uint8_t* budget_unmet, DevPlan* plan,
+                            hipStream_t stream);
 
 // The library's fixed split workspace (a file-scope device array of kernels.hip)
 // on `device`, which must be the current device: its device address and size

@@ -20,6 +20,7 @@
 //               rows into the kept region in every layer, and writes the
 //               eviction mask and compaction indices over the whole cache.
 #include "a2t_internal.h"
+#include "a2t.h"
 
 #include <hip/hip_ext.h>
 #include <math.h>
@@ -995,6 +996,7 @@ __global__ __launch_bounds__(256) void evict_kernel(DevState st, BT b) {
     __shared__ int s_src[256];
     __shared__ int s_dst[256];
     const EvictDesc d = b.d[blockIdx.y];
+    if (d.span == 0) return;   // a device-planned stream that evicts nothing this step
     const int which = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t mb = (int64_t)d.s * st.unit_rows;
@@ -1082,6 +1084,229 @@ __global__ __launch_bounds__(256) void evict_kernel(DevState st, BT b) {
         running += total;
         __syncthreads();
     }
+}
+
+// ------------------------------------------------------ device-planned steps
+// One workgroup: thread i opens the step of stream a.ids[i] from the metadata
+// the caller left in device memory, with the checks a2t_append makes on the
+// host; a stream that fails one records the status (sticky) and takes no part
+// in the step.  The step's q/k/v/o rows sit at a fixed place per listed stream
+// (stream i from row i * max_step_rows).  Thread 0 then plans the key splits:
+// the smallest tile budget per split (>= 2) whose workgroups fit one round of
+// target_wgs and whose partials fit the workspace, as the host planner picks
+// for a single stream.
+__global__ __launch_bounds__(64) void dev_open_kernel(DevState st, DevStepArgs a,
+                                                      const int32_t* n_rows, const int32_t* unit,
+                                                      const uint8_t* seg, const int32_t* pos,
+                                                      DevPlan* plan) {
+    __shared__ int s_n[kMaxDesc];
+    __shared__ int s_R[kMaxDesc];
+    const int i = threadIdx.x;
+    const int MS = st.max_step_rows;
+    if (i < a.count) {
+        const int s = a.ids[i];
+        DevStream& ds = st.dss[s];
+        const int n = n_rows[i], u = unit[i];
+        int err = ds.error;
+        if (!err && ds.step_rows != 0) err = A2T_ERR_STATE;
+        if (!err && (n < 1 || n > MS || u < -1)) err = A2T_ERR_INVALID;
+        if (!err && u == -1 && ds.cur_unit >= 0) err = A2T_ERR_POS;
+        if (!err && ds.cur_unit != -2 && u < ds.cur_unit) err = A2T_ERR_POS;
+        if (!err && (int64_t)ds.ring + n > st.unit_rows) err = A2T_ERR_CAPACITY;
+        int64_t last = ds.last_pos;
+        for (int r = 0; !err && r < n; ++r) {
+            const int sg = seg[(int64_t)i * MS + r];
+            const int p = pos[(int64_t)i * MS + r];
+            if (sg > A2T_SEG_RESPONSE || p < 0 || (u == -1) != (sg == A2T_SEG_PREFIX))
+                err = A2T_ERR_INVALID;
+            else if (p <= last)
+                err = A2T_ERR_POS;
+            last = p;
+        }
+        int slot0 = 0, n_act = 0;
+        if (err) {
+            ds.error = err;
+        } else {
+            slot0 = ds.head + ds.ring;
+            if (slot0 >= st.unit_rows) slot0 -= st.unit_rows;
+            ds.ring += n;
+            ds.step_rows = n;
+            ds.step_slot0 = slot0;
+            ds.cur_unit = ds.cur_unit > u ? ds.cur_unit : u;
+            ds.last_pos = pos[(int64_t)i * MS + n - 1];
+            ds.peak = ds.peak > ds.kept + ds.ring ? ds.peak : ds.kept + ds.ring;
+            ds.budget_unmet = 0;
+            n_act = n;
+        }
+        plan->step[i] = StepDesc{s, n_act, slot0, i * MS};
+        AttnDesc& d = plan->attn[i];
+        d.s = s;
+        d.kept = ds.kept;
+        d.head = ds.head;
+        d.R = ds.kept + ds.ring;
+        d.n_q = n_act;
+        d.rope_row0 = 0;
+        d.n_new = n_act;
+        s_n[i] = n_act;
+        s_R[i] = d.R;
+    }
+    __syncthreads();
+    if (i != 0) return;
+    const int64_t row_floats = st.D + 2;   // split partials of one query row and head
+    int max_tiles = 1;
+    for (int k = 0; k < a.count; ++k)
+        if (s_n[k]) max_tiles = max(max_tiles, (s_R[k] + kTileKeys - 1) / kTileKeys);
+    int budget = max_tiles;
+    for (int b = 2; b <= max_tiles; ++b) {
+        int64_t wgs = 0, ws = 0;
+        for (int k = 0; k < a.count; ++k) {
+            if (!s_n[k]) continue;
+            const int t = max(1, (s_R[k] + kTileKeys - 1) / kTileKeys);
+            const int sp = min((t + b - 1) / b, a.max_splits);
+            wgs += (int64_t)sp * st.Hkv;
+            if (sp > 1) ws += (int64_t)sp * st.Hq * s_n[k] * row_floats;
+        }
+        if (wgs <= a.target_wgs && ws <= st.ws_floats) {
+            budget = b;
+            break;
+        }
+    }
+    int64_t off = 0;
+    for (int k = 0; k < a.count; ++k) {
+        AttnDesc& d = plan->attn[k];
+        d.q_row0 = k * MS;
+        d.in_row0 = k * MS;
+        d.ws_off = off;
+        if (!s_n[k]) {
+            d.splits = 0;   // every workgroup of this stream returns at once
+            d.tile_q = d.tile_r = 0;
+            continue;
+        }
+        const int t = max(1, (s_R[k] + kTileKeys - 1) / kTileKeys);
+        int sp = min((t + budget - 1) / budget, a.max_splits);
+        if (sp > 1 && off + (int64_t)sp * st.Hq * s_n[k] * row_floats > st.ws_floats) sp = 1;
+        d.splits = sp;
+        d.tile_q = t / sp;
+        d.tile_r = t % sp;
+        if (sp > 1) off += (int64_t)sp * st.Hq * s_n[k] * row_floats;
+    }
+}
+
+// One workgroup per listed stream: Sec. 3.3's eviction planned on the device.
+// R > B evicts, oldest first, whole units u <= cur - W that hold acoustic or
+// structural rows, until R <= B or none is left: the shortest prefix of such
+// units whose evictable rows reach R - B (all of them if none does).  The pass
+// covers every ring row of the units up to the last one evicted; the scan ranks
+// the ring's eligible evictable rows with wave ballots and a cross-wave prefix.
+__global__ __launch_bounds__(256) void dev_evict_plan_kernel(DevState st, DevStepArgs a,
+                                                             const int32_t* budget,
+                                                             int32_t* n_evicted,
+                                                             uint8_t* budget_unmet, DevPlan* plan) {
+    __shared__ int s_wave[4];
+    __shared__ int s_cut, s_last, s_span;
+    const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int s = a.ids[i];
+    DevStream& ds = st.dss[s];
+    const int kept = ds.kept, head = ds.head, ring = ds.ring, cur = ds.cur_unit;
+    const int R = kept + ring, B = max(budget[i], 0);   // a negative budget counts as 0
+    const int64_t mb = (int64_t)s * st.unit_rows;
+    auto slot_of = [&](int x) {
+        int slot = head + x;
+        return slot >= st.unit_rows ? slot - st.unit_rows : slot;
+    };
+    EvictDesc e{s, kept, head, R, 0, -2, 0, -1};
+    const bool open = ds.error == 0 && ds.step_rows != 0;
+    int evicted = 0;
+    if (open && R > B) {
+        const int need = R - B;
+        const int64_t limit = (int64_t)cur - a.window;
+        if (tid == 0) {
+            s_cut = -1;
+            s_last = -1;
+        }
+        __syncthreads();
+        // the first eligible evictable row at which the running count reaches
+        // need, else the last eligible evictable row
+        int running = 0;
+        for (int base = 0; base < ring; base += 256) {
+            const int x = base + tid;
+            bool el = false;
+            if (x < ring) {
+                const int slot = slot_of(x);
+                const uint8_t sg = st.unit_seg[mb + slot];
+                el = (sg == A2T_SEG_ACOUSTIC || sg == A2T_SEG_DELIM) && st.unit_uid[mb + slot] <= limit;
+            }
+            const uint64_t bal = __ballot(el);
+            const int below = __popcll(bal & ((1ull << lane) - 1ull));
+            if (lane == 0) s_wave[w] = __popcll(bal);
+            __syncthreads();
+            int before = 0, total = 0;
+            for (int ww = 0; ww < 4; ++ww) {
+                before += ww < w ? s_wave[ww] : 0;
+                total += s_wave[ww];
+            }
+            if (el) {
+                const int rank = running + before + below + 1;   // eligible rows up to x
+                if (rank == need) s_cut = x;
+                if (rank == running + total) s_last = x;          // the chunk's last one
+            }
+            running += total;
+            __syncthreads();
+            if (s_cut >= 0) break;
+        }
+        const int xc = s_cut >= 0 ? s_cut : s_last;
+        if (xc >= 0) {
+            const int ucut = st.unit_uid[mb + slot_of(xc)];
+            // the pass ends at the first ring row of a later unit
+            if (tid == 0) s_span = ring;
+            __syncthreads();
+            for (int base = xc + 1; base < ring; base += 256) {
+                const int x = base + tid;
+                if (x < ring && st.unit_uid[mb + slot_of(x)] > ucut) atomicMin(&s_span, x);
+                __syncthreads();
+                if (s_span < ring) break;
+            }
+            const int span = s_span;
+            // evictable rows inside the pass (all of them are eligible)
+            int cnt = 0;
+            for (int x = tid; x < span; x += 256) {
+                const uint8_t sg = st.unit_seg[mb + slot_of(x)];
+                cnt += (sg == A2T_SEG_ACOUSTIC || sg == A2T_SEG_DELIM);
+            }
+            for (int o = 32; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
+            __syncthreads();
+            if (lane == 0) s_wave[w] = cnt;
+            __syncthreads();
+            evicted = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
+            e.span = span;
+            e.u_last = ucut;
+            e.n_keep = span - evicted;
+            if ((int64_t)kept + e.n_keep > st.kept_rows) {
+                e.span = 0;   // the kept region would overflow: the stream evicts nothing
+                evicted = 0;
+                if (tid == 0) ds.error = A2T_ERR_CAPACITY;
+            }
+        }
+    }
+    __syncthreads();
+    if (tid != 0) return;
+    plan->evict[i] = e;
+    if (open) {
+        if (e.span > 0) {
+            ds.kept = kept + e.n_keep;
+            int h = head + e.span;
+            ds.head = h >= st.unit_rows ? h - st.unit_rows : h;
+            ds.ring = ring - e.span;
+            ds.last_evicted = e.u_last;
+            ds.evicted_total += evicted;
+            ds.moved_total += e.n_keep;
+            ds.last_evict_pre = R;
+        }
+        ds.budget_unmet = R - evicted > B ? 1 : 0;
+        ds.step_rows = 0;
+    }
+    if (n_evicted) n_evicted[i] = evicted;
+    if (budget_unmet) budget_unmet[i] = open && R - evicted > B ? 1 : 0;
 }
 
 // ------------------------------------------------------------- fixed workspace
@@ -1242,6 +1467,77 @@ hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hi
                          static_cast<bf16_t*>(o));
         return hipGetLastError();
     });
+}
+
+// ---- device-planned steps
+hipError_t launch_dev_open(const DevState& st, const DevStepArgs& a, const int32_t* n_rows,
+                           const int32_t* unit, const uint8_t* seg, const int32_t* pos,
+                           DevPlan* plan, hipStream_t stream) {
+    hipLaunchKernelGGL(dev_open_kernel, dim3(1), dim3(64), 0, stream, st, a, n_rows, unit, seg,
+                       pos, plan);
+    return hipGetLastError();
+}
+
+hipError_t launch_step_meta_dev(const DevState& st, const DevPlan* plan, int count,
+                                const uint8_t* seg, const int32_t* pos, const int32_t* unit,
+                                hipStream_t stream) {
+    const DevBatch<StepDesc> b{{plan->step}, 0, 0};
+    hipLaunchKernelGGL((step_meta_kernel<DevBatch<StepDesc>>), dim3(st.max_step_rows, count),
+                       dim3(64), 0, stream, st, b, seg, pos, unit);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_tile_dev(const DevState& st, const DevPlan* plan, int count,
+                                int max_splits, int layer, const void* q, void* o,
+                                const void* k_in, const void* v_in, hipStream_t stream) {
+    const DevBatch<AttnDesc> b{{plan->attn}, layer, st.max_step_rows};
+    const dim3 grid(max_splits * st.Hkv, 1, count);
+    const uint16_t* qq = static_cast<const uint16_t*>(q);
+    uint16_t* oo = static_cast<uint16_t*>(o);
+    const uint16_t* ki = static_cast<const uint16_t*>(k_in);
+    const uint16_t* vi = static_cast<const uint16_t*>(v_in);
+    if (st.D == 128)
+        hipLaunchKernelGGL((attn_tile_kernel<128, DevBatch<AttnDesc>>), grid, dim3(kMfmaThreads), 0,
+                           stream, st, b, qq, oo, ki, vi);
+    else if (st.D == 64)
+        hipLaunchKernelGGL((attn_tile_kernel<64, DevBatch<AttnDesc>>), grid, dim3(kMfmaThreads), 0,
+                           stream, st, b, qq, oo, ki, vi);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_merge_dev(const DevState& st, const DevPlan* plan, int count,
+                                 int max_splits, void* o, hipStream_t stream) {
+    const int G = st.Hq / st.Hkv;
+    if (st.D / 4 * kMergeRows > 256) return hipErrorInvalidValue;
+    const DevBatch<AttnDesc> b{{plan->attn}, 0, st.max_step_rows};
+    const dim3 grid((G * st.max_step_rows + kMergeRows - 1) / kMergeRows * st.Hkv, 1, count);
+    const int nsg = 256 / (kMergeRows * st.D / 4);
+    if ((max_splits + nsg - 1) / nsg > 8)
+        hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 12, DevBatch<AttnDesc>>), grid, dim3(256), 0,
+                           stream, st, b, static_cast<bf16_t*>(o));
+    else
+        hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 8, DevBatch<AttnDesc>>), grid, dim3(256), 0,
+                           stream, st, b, static_cast<bf16_t*>(o));
+    return hipGetLastError();
+}
+
+hipError_t launch_dev_evict(const DevState& st, const DevStepArgs& a, const int32_t* budget,
+                            int32_t* n_evicted, uint8_t* budget_unmet, DevPlan* plan,
+                            hipStream_t stream) {
+    hipLaunchKernelGGL(dev_evict_plan_kernel, dim3(a.count), dim3(256), 0, stream, st, a, budget,
+                       n_evicted, budget_unmet, plan);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const DevBatch<EvictDesc> b{{plan->evict}, 0, 0};
+    if (st.dtype == 0)
+        hipLaunchKernelGGL((evict_kernel<4, DevBatch<EvictDesc>>), dim3(st.L + 1, a.count), dim3(256),
+                           0, stream, st, b);
+    else
+        hipLaunchKernelGGL((evict_kernel<2, DevBatch<EvictDesc>>), dim3(st.L + 1, a.count), dim3(256),
+                           0, stream, st, b);
+    return hipGetLastError();
 }
 
 hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream,

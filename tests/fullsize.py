@@ -40,12 +40,18 @@ from tests.harness import Mismatch, bf16_bits_to_f32, make_cache
 class SampledBatch:
     def __init__(self, cfg, seed, specs, *, sampled, layers_checked, budgets, window, unit_rows,
                  kept_rows, max_step, tol, check_every=1, check_steps=None, listen_call="fused",
-                 decode_call="decode", evict=True, oracle="lockstep", label=""):
+                 decode_call="decode", evict=True, oracle="lockstep", label="", rule=None,
+                 n_sink=0):
         import torch
         import paper_2609_31224_amd as a2t
         from oracle.cache import OracleCache
+        from oracle.policy import EvictRule
         from oracle.replay import MetadataReplay, replay_metadata
         self.torch, self.a2t = torch, a2t
+        # eviction rule: None = a2t_evict (Sec. 3.3), else "row" / "sink_recent"
+        # through a2t_evict_rule
+        self.rule, self.n_sink = rule, n_sink
+        self.oracle_rule = EvictRule(rule or "unit", n_sink)
         self.cfg, self.seed, self.specs = cfg, seed, specs
         self.sampled = list(sampled)
         self.layers_checked = list(layers_checked)
@@ -61,10 +67,10 @@ class SampledBatch:
         self.oracles = {} if self.rebuild else {
             i: OracleCache(cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, self.layers_checked,
                            theta=cfg.rope_theta, scale=cfg.scale) for i in self.sampled}
-        self.traces = [replay_metadata(s, b, window, evict=evict)
+        self.traces = [replay_metadata(s, b, window, evict=evict, rule=self.oracle_rule)
                        for s, b in zip(specs, self.budgets)]
         # step-by-step replays that also give each step's mask and compaction indices
-        self.replays = [MetadataReplay(s, b, window, record_masks=True)
+        self.replays = [MetadataReplay(s, b, window, record_masks=True, rule=self.oracle_rule)
                         for s, b in zip(specs, self.budgets)] if evict else None
         self.moved = [0] * len(specs)
         self.mask_checks = 0
@@ -173,7 +179,13 @@ class SampledBatch:
             return
         if self.evict:
             budgets = [self.budgets[i] for i in ids]
-            n_ev, unmet = a2t.a2t_evict(self.cache, ids, budgets, self.window)
+            if self.rule is None:
+                n_ev, unmet = a2t.a2t_evict(self.cache, ids, budgets, self.window)
+            else:
+                n_ev, unmet = a2t.a2t_evict_rule(
+                    self.cache, ids, budgets, self.window,
+                    {"row": a2t.A2T_RULE_ROW, "sink_recent": a2t.A2T_RULE_SINK_RECENT}[self.rule],
+                    self.n_sink)
         else:
             n_ev, unmet = np.zeros(len(ids), np.int32), np.zeros(len(ids), np.uint8)
         for j, (i, st) in enumerate(act):
@@ -187,7 +199,7 @@ class SampledBatch:
             if self.replays:
                 self._check_eviction(t, i, rtr[i], want)
             if i in self.oracles and self.evict:
-                rec = self.oracles[i].evict(self.budgets[i], self.window)
+                rec = self.oracles[i].evict(self.budgets[i], self.window, self.oracle_rule)
                 assert rec.n_evicted == want
         if self.rebuild:
             self.oracles = {}

@@ -165,3 +165,32 @@ def test_budget_sweep_fifteen_ten_minute_sessions(gpu):
     for B in (8000, 6000, 4000):
         assert B - 19 < res[B][0] <= B < res[B][1] <= B + cfg.max_unit_rows
     assert res[None][0] == res[None][1] > res[8000][1] > res[6000][1] > res[4000][1] > res[0][1]
+
+
+@pytest.mark.parametrize("rule,budget,n_sink", [("row", 4000, 0), ("sink_recent", 2004, 4)])
+def test_rule_variants_fifteen_ten_minute_sessions(gpu, rule, budget, n_sink):
+    """The two variants of the rule on the budget sweep's 15 sessions at full
+    size: every session's eviction counts, flags, masks, compaction indices and
+    kept-region moves at every step, End, Peak and the final layout, against
+    the oracle's replay of the same rule (Sec. 3.3 granularity ablation; the
+    StreamingLLM comparison of Table 1: 4 sinks + 2,000 recent rows)."""
+    from synth.streams import make_sessions
+    cfg = CONFIGS[1]
+    specs = make_sessions(cfg, range(1, 16)).streams
+    total = max(s.total_rows() for s in specs)
+    kept = max(row_bounds(s)[1] for s in specs) + 64
+    run = SampledBatch(cfg, 1, specs, sampled=[], layers_checked=[0], budgets=[budget] * len(specs),
+                       window=cfg.window, unit_rows=total + 64, kept_rows=kept,
+                       max_step=cfg.max_unit_rows, tol=BF16_TOL, check_steps=set(),
+                       listen_call="fill", label=f"{rule} B={budget}", rule=rule, n_sink=n_sink)
+    try:
+        run.run(progress_every=0)
+        ends = [tr.steps[-1].n_post for tr in run.traces]
+        peaks = [tr.peak for tr in run.traces]
+    finally:
+        run.close()
+    print(f"[{rule}] budget {budget}: End {np.mean(ends):.1f} Peak {np.mean(peaks):.1f}, "
+          f"{run.mask_checks} mask checks", flush=True)
+    assert run.mask_checks > 15 * 300
+    # both variants meet their budget exactly whenever they evict
+    assert all(e == budget for e in ends)
