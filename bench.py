@@ -1258,6 +1258,20 @@ def run_distill(args):
         lib.a2t_distill_profile_enable(d.ptr, 0)
         kern[name] = {"launches": nl.value, "avg_us": ms.value * 1e3 / max(1, nl.value)}
     a2t.a2t_distill_destroy(d)
+    # a streaming floor for the same bytes: one elementwise pass that reads both
+    # logit arrays once and writes one array of the same size (torch's add), the
+    # traffic a single-pass evaluation with the gradient would move
+    st_v, grad_v = st[:, :vocab], grad[:, :vocab]
+    for _ in range(3):
+        torch.add(st_v, te, out=grad_v)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        torch.add(st_v, te, out=grad_v)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    floor_us = ev0.elapsed_time(ev1) * 1e3 / args.steps
+    floor_bytes = 3 * n * vocab * 2
     # algorithmic bytes of one evaluation: read both logit rows once, write the gradient once
     alg = n * ((vocab + added) * 2 + vocab * 2 + (vocab + added) * 2)
     alg_loss = n * ((vocab + added) * 2 + vocab * 2)
@@ -1298,6 +1312,10 @@ def run_distill(args):
                       "alg_bytes_per_launch": alg_loss,
                       "achieved_gbps": alg_loss / (kern["distill_row_loss_only"]["avg_us"] * 1e-6) / 1e9},
         "kernels_us": kern,
+        "single_pass_floor": {"kernel": "torch.add of the two logit arrays into a third",
+                              "avg_us": floor_us, "bytes": floor_bytes,
+                              "gbps": floor_bytes / (floor_us * 1e-6) / 1e9,
+                              "distill_row_over_floor": us / floor_us},
         "unit_ms": {"mean": float(step_ms.mean()), "p50": float(np.percentile(step_ms, 50)),
                     "p99": float(np.percentile(step_ms, 99))},
         "cpu_baseline": base_line,
