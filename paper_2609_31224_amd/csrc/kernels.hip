@@ -901,23 +901,19 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 // over more workgroups than one thread per four outputs would: the partials
 // come from memory and a CU streams only so many bytes per microsecond.  The
 // order of every sum is fixed, so the result is deterministic.
-template <typename T, int B, class BT>
-__global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
+// One row group (kMergeRows query rows of KV head g) of the merge; every thread
+// of the workgroup calls it (one barrier inside).
+template <typename T, int B>
+__device__ __forceinline__ void merge_row_group(const DevState& st, const AttnDesc& d, T* o, int g,
+                                                int rg, float4* s_o, float2* s_ml) {
     constexpr int MR = kMergeRows;
-    __shared__ float4 s_o[256];
-    __shared__ float2 s_ml[256];
-    const AttnDesc d = b.d[blockIdx.z];
-    if (d.splits <= 1) return;
-    // row group rg of KV head g is linear block rg * Hkv + g: the XCD of head g,
-    // like the attention workgroups that wrote its partials
-    const int G = st.G, M = G * d.n_q, D = st.D, g = blockIdx.x % st.Hkv, rg = blockIdx.x / st.Hkv;
+    const int G = st.G, M = G * d.n_q, D = st.D;
     const int tpr = D / 4;          // threads per query row
     const int tsg = MR * tpr;       // threads per split group
     const int nsg = 256 / tsg;      // split groups
     const int sg = threadIdx.x / tsg, r = threadIdx.x - sg * tsg;
     const int rr = r / tpr, d4 = (r - rr * tpr) * 4;
     const int mq = rg * MR + rr;
-    if (rg * MR >= M) return;  // the whole workgroup is past the rows
     const bool live = mq < M;
     const int mqc = live ? mq : M - 1;
     const float* po = st.ws + d.ws_off;
@@ -982,6 +978,24 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o
     T* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D + d4;
 #pragma unroll
     for (int e = 0; e < 4; ++e) Elt<T>::store(op + e, Ot[e] * inv);
+}
+
+template <typename T, int B, class BT>
+__global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
+    __shared__ float4 s_o[256];
+    __shared__ float2 s_ml[256];
+    const AttnDesc d = b.d[blockIdx.z];
+    if (d.splits <= 1) return;
+    // row group rg of KV head g is linear block rg * Hkv + g: the XCD of head g,
+    // like the attention workgroups that wrote its partials.  A grid with fewer
+    // row groups than the step has (device-planned steps, whose grid is fixed)
+    // strides over them.
+    const int g = blockIdx.x % st.Hkv, groups = gridDim.x / st.Hkv;
+    const int M = st.G * d.n_q;
+    for (int rg = blockIdx.x / st.Hkv; rg * kMergeRows < M; rg += groups) {
+        merge_row_group<T, B>(st, d, o, g, rg, s_o, s_ml);
+        __syncthreads();   // s_o / s_ml are reused by the next row group
+    }
 }
 
 // ---------------------------------------------------------------------- evict
@@ -1087,6 +1101,8 @@ __global__ __launch_bounds__(256) void evict_kernel(DevState st, BT b) {
 }
 
 // ------------------------------------------------------ device-planned steps
+constexpr int kDevMergeGroups = 32;   // merge workgroups per KV head of a device-planned launch
+
 // One workgroup: thread i opens the step of stream a.ids[i] from the metadata
 // the caller left in device memory, with the checks a2t_append makes on the
 // host; a stream that fails one records the status (sticky) and takes no part
@@ -1512,7 +1528,9 @@ hipError_t launch_attn_merge_dev(const DevState& st, const DevPlan* plan, int co
     const int G = st.Hq / st.Hkv;
     if (st.D / 4 * kMergeRows > 256) return hipErrorInvalidValue;
     const DevBatch<AttnDesc> b{{plan->attn}, 0, st.max_step_rows};
-    const dim3 grid((G * st.max_step_rows + kMergeRows - 1) / kMergeRows * st.Hkv, 1, count);
+    // at most kDevMergeGroups row groups per head; the kernel strides over the rest
+    const int groups = std::min((G * st.max_step_rows + kMergeRows - 1) / kMergeRows, kDevMergeGroups);
+    const dim3 grid(groups * st.Hkv, 1, count);
     const int nsg = 256 / (kMergeRows * st.D / 4);
     if ((max_splits + nsg - 1) / nsg > 8)
         hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 12, DevBatch<AttnDesc>>), grid, dim3(256), 0,

@@ -103,8 +103,10 @@ def test_config3_full_decode_batched(gpu, decode_call):
 def test_config4_full_hour_long_with_control(gpu):
     # 16 streams x 3600 units (budget 8192, window 60), then the same streams with no
     # eviction (control, ~79 K resident rows each: ~188 GB of K/V in one cache).  Every
-    # stream's eviction counts, budget flags, final layout and peak are checked; attention
-    # of a sampled stream on the last layer at three steps, against a rebuilt oracle.
+    # stream's eviction counts, budget flags, every eviction's mask and compaction
+    # indices, final layout and peak are checked; attention against a rebuilt oracle on
+    # two sampled streams: layers 0, 17 and 35 at ten steps spread over the hour with
+    # eviction, the last layer at three steps in the control (~79 K-row histories).
     cfg = CONFIGS[4]
     specs = make_workload(cfg).streams
     T = max(len(s.steps) for s in specs)
@@ -116,11 +118,15 @@ def test_config4_full_hour_long_with_control(gpu):
             unit_rows = max(s.total_rows() for s in specs) + 64
             kept, max_n = 64, cfg.max_unit_rows
         label = "cfg4 full " + ("evict" if evict else "control")
-        run = SampledBatch(cfg, cfg.index, specs, sampled=[5], layers_checked=[35],
+        if evict:
+            layers, steps = [0, 17, 35], {(k + 1) * T // 10 - 1 for k in range(10)}
+        else:
+            layers, steps = [35], {T // 3 - 1, 2 * T // 3 - 1, T - 1}
+        run = SampledBatch(cfg, cfg.index, specs, sampled=[5, 12], layers_checked=layers,
                            budgets=[cfg.budget] * len(specs), window=cfg.window,
                            unit_rows=unit_rows, kept_rows=kept, max_step=max_n, tol=BF16_TOL,
-                           check_steps={T // 3 - 1, 2 * T // 3 - 1, T - 1},
-                           listen_call="fill_check", evict=evict, oracle="rebuild", label=label)
+                           check_steps=steps, listen_call="fill_check", evict=evict,
+                           oracle="rebuild", label=label)
         try:
             run.run(progress_every=300)
             peaks[evict] = max(tr.peak for tr in run.traces)
@@ -130,7 +136,7 @@ def test_config4_full_hour_long_with_control(gpu):
               f"mask checks {run.mask_checks}, attention checks {run.attn_checks}, "
               f"max err {run.max_err:.3e}, peak rows {peaks[evict]}", flush=True)
         assert run.mask_checks == (run.evictions if evict else 0)
-        assert run.attn_checks == 3
+        assert run.attn_checks == (2 * 3 * 10 if evict else 2 * 3)
         if evict:
             assert run.unmet_steps > 0 and run.evictions > 16 * 3000
     reduction = 1.0 - peaks[True] / peaks[False]
