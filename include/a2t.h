@@ -308,7 +308,8 @@ int a2t_evict_rule(a2t_cache* c, int32_t n_streams, const int32_t* stream_ids,
  * (rows, ring head, newest unit and position, the per-unit eviction plan): the
  * host-planned calls (a2t_append*, a2t_*_attn, a2t_evict*, a2t_stream_info_get,
  * a2t_read_*) return A2T_ERR_STATE.  Only bf16 caches (the fused MFMA path);
- * at most 64 streams per step; eviction follows Sec. 3.3's whole-unit rule.
+ * at most 64 streams per step; eviction follows Sec. 3.3's whole-unit rule
+ * (a2t_dev_evict) or a variant of it (a2t_dev_evict_rule).
  * ------------------------------------------------------------------------- */
 
 /* Hand the host's per-stream state to the device (synchronises).  Errors:
@@ -356,6 +357,18 @@ int a2t_dev_append_attn(a2t_cache* c, int32_t layer, const void* k, const void* 
  * reported by a2t_dev_end (CAPACITY) and that stream evicts nothing. */
 int a2t_dev_evict(a2t_cache* c, const int32_t* budget, int32_t window, int32_t* n_evicted,
                   uint8_t* budget_unmet);
+
+/* a2t_dev_evict with a choice of rule (a2t_rule, as in a2t_evict_rule) and,
+ * for A2T_RULE_SINK_RECENT, the sink count (>= 0; ignored by the other rules).
+ * The rule's conditions on the device values are checked per stream on the
+ * device: a budget below n_sink (A2T_ERR_INVALID) or a kept region holding
+ * rows other than the sinks (A2T_ERR_STATE) is recorded for that stream like
+ * a2t_dev_open's checks (reported by a2t_dev_end; the stream evicts nothing
+ * and takes no part in later device-planned steps).  Errors (host-side,
+ * nothing enqueued): INVALID (unknown rule, n_sink < 0, and those of
+ * a2t_dev_evict), STATE. */
+int a2t_dev_evict_rule(a2t_cache* c, const int32_t* budget, int32_t window, int32_t rule,
+                       int32_t n_sink, int32_t* n_evicted, uint8_t* budget_unmet);
 
 /* Bookkeeping of one stream (host state, no synchronisation). */
 int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out);

@@ -39,7 +39,7 @@ EXPORTED = (
     "a2t_cache_create", "a2t_cache_destroy", "a2t_set_stream", "a2t_append",
     "a2t_chunk_attn", "a2t_append_attn", "a2t_append_attn_noalloc", "a2t_decode_attn",
     "a2t_evict", "a2t_evict_rule", "a2t_dev_begin", "a2t_dev_end", "a2t_dev_open",
-    "a2t_dev_append_attn", "a2t_dev_evict",
+    "a2t_dev_append_attn", "a2t_dev_evict", "a2t_dev_evict_rule",
     "a2t_stream_info_get",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
     "a2t_profile_enable", "a2t_kernel_time", "a2t_profile_reserve", "a2t_status_str",
@@ -101,6 +101,7 @@ def _load():
         "a2t_dev_open": (C.c_int, [VP, I32, P(I32), VP, VP, VP, VP]),
         "a2t_dev_append_attn": (C.c_int, [VP, I32, VP, VP, VP, VP]),
         "a2t_dev_evict": (C.c_int, [VP, VP, I32, VP, VP]),
+        "a2t_dev_evict_rule": (C.c_int, [VP, VP, I32, I32, I32, VP, VP]),
         "a2t_stream_info_get": (C.c_int, [VP, I32, P(a2t_stream_info)]),
         "a2t_read_layout": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
         "a2t_read_last_evict": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
@@ -340,6 +341,14 @@ def a2t_dev_evict(c: Cache, budget, window: int, n_evicted=None, budget_unmet=No
     rc = _lib.a2t_dev_evict(c.ptr, _dev(budget, "budget"), window, _dev(n_evicted, "n_evicted"),
                             _dev(budget_unmet, "budget_unmet"))
     _check(rc, "a2t_dev_evict")
+
+
+def a2t_dev_evict_rule(c: Cache, budget, window: int, rule: int, n_sink: int = 0, n_evicted=None,
+                       budget_unmet=None) -> None:
+    """a2t_dev_evict with an a2t_rule (A2T_RULE_*) and, for the sink rule, the sink count."""
+    rc = _lib.a2t_dev_evict_rule(c.ptr, _dev(budget, "budget"), window, rule, n_sink,
+                                 _dev(n_evicted, "n_evicted"), _dev(budget_unmet, "budget_unmet"))
+    _check(rc, "a2t_dev_evict_rule")
 
 
 def a2t_stream_info_get(c: Cache, stream: int) -> dict:

@@ -463,6 +463,45 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         d.ws_off = off;
         if (d.splits > 1) off += (int64_t)d.splits * c->cfg.n_kv_heads * G * d.n_q * (c->cfg.head_dim + 2);
     }
+    // a fused step's own rows: when the launch's workgroups (with one more split
+    // per tile holding them) still fit one round over the CUs, those tiles get
+    // one-tile splits of their own, so that the workgroup that also rotates and
+    // stores the rows is not the last of the launch to finish
+    if (in_row0 && !wsc) {
+        const int Hkv = c->cfg.n_kv_heads;
+        int64_t wgs = 0, ws = 0;
+        int32_t tq[kMaxDesc], tr[kMaxDesc], ns[kMaxDesc];
+        bool any = false;
+        for (int k = 0; k < n; ++k) {
+            const AttnDesc& d = b.d[k];
+            const int n_tiles = (d.R + kTileKeys - 1) / kTileKeys;
+            const int qmax = (n_tiles + d.splits - 1) / d.splits;
+            const int t_old = (d.R - d.n_new) / kTileKeys, m = n_tiles - t_old;
+            tq[k] = d.tile_q, tr[k] = d.tile_r, ns[k] = d.splits;
+            if (d.splits > 1 && qmax >= 2 && d.n_new > 0 && t_old >= 1 && m >= 1) {
+                const int s_old = (t_old + qmax - 1) / qmax;
+                if (s_old + m <= kMaxSplits) {
+                    ns[k] = s_old + m;
+                    tq[k] = t_old / s_old;
+                    tr[k] = (t_old % s_old) | (m << 16);
+                    any = true;
+                }
+            }
+            wgs += (int64_t)ns[k] * Hkv;
+            if (ns[k] > 1) ws += (int64_t)ns[k] * Hkv * G * d.n_q * (c->cfg.head_dim + 2);
+        }
+        if (any && wgs <= c->target_wgs && ws <= c->dev.ws_floats) {
+            int64_t o2 = 0;
+            for (int k = 0; k < n; ++k) {
+                AttnDesc& d = b.d[k];
+                d.splits = ns[k], d.tile_q = tq[k], d.tile_r = tr[k];
+                d.ws_off = o2;
+                if (d.splits > 1) o2 += (int64_t)d.splits * Hkv * G * d.n_q * (c->cfg.head_dim + 2);
+                splits = std::max(splits, (int)d.splits);
+            }
+            off = o2;
+        }
+    }
     b.max_splits = splits;
     b.max_rows = max_rows;
     // bf16 caches use the MFMA kernel for decode too: with one query row per
@@ -1482,15 +1521,24 @@ int a2t_dev_append_attn(a2t_cache* c, int32_t layer, const void* k, const void* 
 
 int a2t_dev_evict(a2t_cache* c, const int32_t* budget, int32_t window, int32_t* n_evicted,
                   uint8_t* budget_unmet) {
+    return a2t_dev_evict_rule(c, budget, window, A2T_RULE_UNIT, 0, n_evicted, budget_unmet);
+}
+
+int a2t_dev_evict_rule(a2t_cache* c, const int32_t* budget, int32_t window, int32_t rule,
+                       int32_t n_sink, int32_t* n_evicted, uint8_t* budget_unmet) {
     if (!c) return A2T_ERR_INVALID;
     if (c->poisoned) return A2T_ERR_HIP;
     if (!c->dev_mode || !c->dev_step_open) return A2T_ERR_STATE;
-    if (!budget || window < 0) return A2T_ERR_INVALID;
+    if (!budget || window < 0 || n_sink < 0) return A2T_ERR_INVALID;
+    if (rule != A2T_RULE_UNIT && rule != A2T_RULE_ROW && rule != A2T_RULE_SINK_RECENT)
+        return A2T_ERR_INVALID;
     for (uint8_t l : c->dev_layers)
         if (!l) return A2T_ERR_STATE;
     DevStepArgs a{};
     a.count = c->dev_count;
     a.window = window;
+    a.rule = rule;
+    a.n_sink = rule == A2T_RULE_SINK_RECENT ? n_sink : 0;
     std::copy(c->dev_ids, c->dev_ids + c->dev_count, a.ids);
     DeviceGuard dg(c->cfg.device);
     if (launch_dev_evict(c->dev, a, budget, n_evicted, budget_unmet, c->dplan, c->stream) != hipSuccess)

@@ -109,8 +109,9 @@ struct AttnDesc {
     int32_t splits;    // key splits; 1 = write o directly
     int32_t n_new;     // fused append: the last n_new keys come from the input k/v (else 0)
     int32_t in_row0;   // fused append: first row of this stream in the input k/v
-    int32_t tile_q;    // key tiles per split: split sp takes tile_q tiles, one more if
-    int32_t tile_r;    //   sp < tile_r, starting at tile sp * tile_q + min(sp, tile_r)
+    int32_t tile_q;    // key tiles per split: split sp < splits - m takes tile_q tiles,
+    int32_t tile_r;    //   one more if sp < r, from tile sp * tile_q + min(sp, r); the last
+                       //   m splits take one tile each (r = tile_r & 0xffff, m = tile_r >> 16)
     int64_t ws_off;    // float offset of this stream's partials in the workspace
 };
 template <int N>
@@ -175,6 +176,8 @@ struct DevStepArgs {
     int32_t max_splits;   // key splits the attention grid was sized for
     int32_t target_wgs;   // workgroups one attention launch spreads over at most
     int32_t window;       // recent units protected (eviction)
+    int32_t rule;         // a2t_rule of the eviction
+    int32_t n_sink;       // sink rows (A2T_RULE_SINK_RECENT)
     int32_t ids[kMaxDesc];
 };
 

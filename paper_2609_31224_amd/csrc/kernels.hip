@@ -512,7 +512,11 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
     if (sp >= d.splits) return;
     const int G = st.G, nq = d.n_q, M = G * nq, R = d.R;
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, l16 = lane & 15, lg = lane >> 4;
-    const int t0 = sp * d.tile_q + min(sp, d.tile_r), t1 = t0 + d.tile_q + (sp < d.tile_r ? 1 : 0);
+    // split sp takes tile_q tiles, one more if sp < r; the last m splits take one
+    // tile each (r = tile_r & 0xffff, m = tile_r >> 16)
+    const int r1 = d.tile_r & 0xffff, cut = d.splits - (d.tile_r >> 16);
+    const int t0 = sp < cut ? sp * d.tile_q + min(sp, r1) : cut * d.tile_q + min(cut, r1) + (sp - cut);
+    const int t1 = sp < cut ? t0 + d.tile_q + (sp < r1 ? 1 : 0) : t0 + 1;
     const int vis0 = R - nq;
     const int kept = d.kept, head = d.head, ring_rows = st.unit_rows;
     const int newbase = R - d.n_new;  // fused append: rows newbase .. R-1 come from k_in / v_in
@@ -1233,7 +1237,26 @@ __global__ __launch_bounds__(256) void dev_evict_plan_kernel(DevState st, DevSte
     EvictDesc e{s, kept, head, R, 0, -2, 0, -1};
     const bool open = ds.error == 0 && ds.step_rows != 0;
     int evicted = 0;
-    if (open && R > B) {
+    if (open && R > B && a.rule == A2T_RULE_SINK_RECENT) {
+        // every row but the n_sink oldest and the B - n_sink newest: the pass covers
+        // the ring's remaining sinks and the R - B rows after them
+        const int n_sink = a.n_sink;
+        if (B < n_sink || kept > n_sink) {
+            if (tid == 0) ds.error = B < n_sink ? A2T_ERR_INVALID : A2T_ERR_STATE;
+        } else {
+            const int sinks_left = n_sink - kept;
+            e.span = sinks_left + (R - B);   // <= ring, since B >= n_sink >= kept
+            e.u_last = st.unit_uid[mb + slot_of(e.span - 1)];
+            e.n_keep = sinks_left;
+            e.sink = n_sink;
+            evicted = R - B;
+            if ((int64_t)kept + e.n_keep > st.kept_rows) {
+                e.span = 0;
+                evicted = 0;
+                if (tid == 0) ds.error = A2T_ERR_CAPACITY;
+            }
+        }
+    } else if (open && R > B) {
         const int need = R - B;
         const int64_t limit = (int64_t)cur - a.window;
         if (tid == 0) {
@@ -1273,10 +1296,11 @@ __global__ __launch_bounds__(256) void dev_evict_plan_kernel(DevState st, DevSte
         const int xc = s_cut >= 0 ? s_cut : s_last;
         if (xc >= 0) {
             const int ucut = st.unit_uid[mb + slot_of(xc)];
-            // the pass ends at the first ring row of a later unit
-            if (tid == 0) s_span = ring;
+            // whole units: the pass ends at the first ring row of a later unit; per
+            // row: at the newest evicted row itself
+            if (tid == 0) s_span = a.rule == A2T_RULE_ROW ? xc + 1 : ring;
             __syncthreads();
-            for (int base = xc + 1; base < ring; base += 256) {
+            for (int base = xc + 1; a.rule != A2T_RULE_ROW && base < ring; base += 256) {
                 const int x = base + tid;
                 if (x < ring && st.unit_uid[mb + slot_of(x)] > ucut) atomicMin(&s_span, x);
                 __syncthreads();

@@ -26,11 +26,16 @@ class DevRun:
     layers; other layers reuse the first checked layer's values."""
 
     def __init__(self, cfg, seed, specs, budgets, window, layers_checked, n_layers, unit_rows,
-                 kept_rows, max_step):
+                 kept_rows, max_step, rule=None, n_sink=0):
         import torch
         import paper_2609_31224_amd as a2t
         from oracle.cache import OracleCache
+        from oracle.policy import EvictRule
         self.torch, self.a2t = torch, a2t
+        # eviction rule: None = a2t_dev_evict (Sec. 3.3's whole-unit rule), else
+        # "unit" / "row" / "sink_recent" through a2t_dev_evict_rule
+        self.rule, self.n_sink = rule, n_sink
+        self.oracle_rule = EvictRule(rule or "unit", n_sink)
         self.cfg, self.seed, self.specs = cfg, seed, specs
         self.budgets, self.window = budgets, window
         self.layers_checked, self.L = list(layers_checked), n_layers
@@ -98,7 +103,13 @@ class DevRun:
         for layer in range(self.L):
             a2t.a2t_dev_append_attn(self.cache, layer, self.k[layer], self.v[layer], self.q[layer],
                                     self.o[layer])
-        a2t.a2t_dev_evict(self.cache, self.budget, self.window, self.n_ev, self.unmet)
+        if self.rule is None:
+            a2t.a2t_dev_evict(self.cache, self.budget, self.window, self.n_ev, self.unmet)
+        else:
+            lib_rule = {"unit": a2t.A2T_RULE_UNIT, "row": a2t.A2T_RULE_ROW,
+                        "sink_recent": a2t.A2T_RULE_SINK_RECENT}[self.rule]
+            a2t.a2t_dev_evict_rule(self.cache, self.budget, self.window, lib_rule, self.n_sink,
+                                   self.n_ev, self.unmet)
 
     def check(self, full):
         """Attention of step t against the oracle; with ``full`` also the
@@ -117,7 +128,7 @@ class DevRun:
                     raise Mismatch(f"step {t} stream {i} layer {layer}: attention max err {err}")
         n_ev = self.n_ev.cpu().numpy()
         unmet = self.unmet.cpu().numpy()
-        recs = [o.evict(b, self.window) for o, b in zip(self.oracles, self.budgets)]
+        recs = [o.evict(b, self.window, self.oracle_rule) for o, b in zip(self.oracles, self.budgets)]
         for i, rec in enumerate(recs):
             if int(n_ev[i]) != rec.n_evicted or bool(unmet[i]) != rec.plan.budget_unmet:
                 raise Mismatch(f"step {t} stream {i}: evicted {n_ev[i]}/{rec.n_evicted} "
@@ -172,6 +183,82 @@ def test_device_planned_config0_shape(gpu):
         run.close()
     print(f"[device cfg0] evictions={run.evictions} max_err={run.max_err:.3e}", flush=True)
     assert run.evictions > 60
+
+
+@pytest.mark.parametrize("rule,n_sink,budgets", [("unit", 0, (None, 200, 300)),
+                                                   ("row", 0, (None, 200, 300)),
+                                                   ("row", 0, (1, 57, 123)),
+                                                   ("sink_recent", 4, (None, 200, 64)),
+                                                   ("sink_recent", 0, (30, 7, 1)),
+                                                   ("sink_recent", 17, (17, 40, 100))])
+def test_device_planned_rule_variants_config0(gpu, rule, n_sink, budgets):
+    """The variants of the rule planned on the device (a2t_dev_evict_rule):
+    config 0's stream structure with two more streams, every step checked in
+    full against the oracle's replay of the same rule (layout, mask and
+    compaction indices bit-exact, stored K/V, attention).  Budgets include the
+    sink count itself (nothing but sinks and recent rows) and tiny budgets that
+    evict at almost every step."""
+    cfg = CONFIGS[0]
+    specs = [make_workload(cfg, seed=s).streams[0] for s in (0, 4, 7)]
+    budgets = [cfg.budget if b is None else b for b in budgets]
+    run = DevRun(cfg, 0, specs, budgets, cfg.window, [0], 1, rule=rule, n_sink=n_sink,
+                 **_bounds(specs))
+    import paper_2609_31224_amd as a2t
+    try:
+        a2t.a2t_dev_begin(run.cache)
+        for t in range(len(specs[0].steps)):
+            run.fill(t)
+            run.issue()
+            run.check(full=True)
+        a2t.a2t_dev_end(run.cache)
+    finally:
+        run.close()
+    print(f"[device {rule} sinks {n_sink} budgets {budgets}] evictions={run.evictions} "
+          f"max_err={run.max_err:.3e}", flush=True)
+    assert run.evictions > 40
+
+
+def test_device_planned_sink_rule_errors(gpu):
+    """A budget below the sink count is refused on the device for that stream
+    only (A2T_ERR_INVALID from a2t_dev_end, nothing evicted); the other stream
+    evicts as the host-planned rule does."""
+    import paper_2609_31224_amd as a2t
+    cfg = CONFIGS[0]
+    specs = [tiny_stream([[1, 1, 3]] * 6), tiny_stream([[1, 1, 2]] * 6)]
+    run = DevRun(cfg, 2, specs, [3, 6], 1, [0], 1, unit_rows=64, kept_rows=16, max_step=8,
+                 rule="sink_recent", n_sink=4)
+    try:
+        a2t.a2t_dev_begin(run.cache)
+        for t in range(3):
+            run.fill(t)
+            run.issue()
+        run.torch.cuda.synchronize()
+        # step 1 took stream 0 over its budget of 3 < 4 sinks: refused, and the
+        # stream sits out step 2; stream 1 went from 9 to 6 rows at step 2
+        assert run.n_ev.cpu().tolist() == [0, 3]
+        # an open step: an unknown rule or a negative sink count is refused on
+        # the host, nothing enqueued, and the step stays open
+        run.fill(3)
+        a2t.a2t_dev_open(run.cache, [0, 1], run.n_rows, run.unit, run.seg, run.pos)
+        a2t.a2t_dev_append_attn(run.cache, 0, run.k[0], run.v[0], run.q[0], run.o[0])
+        for rule, sinks in ((7, 0), (a2t.A2T_RULE_SINK_RECENT, -1)):
+            with pytest.raises(a2t.A2TError) as e:
+                a2t.a2t_dev_evict_rule(run.cache, run.budget, 1, rule, sinks)
+            assert e.value.status == a2t.A2T_ERR_INVALID
+        a2t.a2t_dev_evict_rule(run.cache, run.budget, 1, a2t.A2T_RULE_SINK_RECENT, 4, run.n_ev,
+                               run.unmet)
+        run.torch.cuda.synchronize()
+        assert run.n_ev.cpu().tolist() == [0, 3]
+        with pytest.raises(a2t.A2TError) as e:
+            a2t.a2t_dev_end(run.cache)
+        assert e.value.status == a2t.A2T_ERR_INVALID
+        assert a2t.a2t_stream_info_get(run.cache, 0)["resident"] == 6
+        assert a2t.a2t_stream_info_get(run.cache, 1)["resident"] == 6
+        p, _, _ = a2t.a2t_read_layout(run.cache, 1)
+        # the four sinks, then the budget's two newest rows
+        assert p.tolist() == [0, 1, 2, 3, 10, 11]
+    finally:
+        run.close()
 
 
 def test_device_planned_edge_streams(gpu):
