@@ -199,6 +199,37 @@ def cpu_baseline_slice(cfg, seed, picks, n_steps, unit):
                       f"x all {cfg.n_layers} layers, fp64 numpy; {dt:.1f} s of CPU work"}
 
 
+def cpu_baseline_steps(cfg, seed, spec, k0, n_steps, n_units, sample_layers):
+    """The float64 oracle on steps k0 .. k0 + n_steps - 1 of one stream (``n_units``
+    units of a workload whose units take several calls), append + attention on
+    the first ``sample_layers`` layers and the eviction check where a step
+    carries it, scaled to all layers.  Rate = units per second."""
+    from oracle.replay import resume
+    sample_layers = max(1, min(sample_layers, cfg.n_layers))
+    layers = list(range(sample_layers))
+    cache = resume(cfg, seed, spec, spec.budget, cfg.window, k0, layers)
+    vals = [step_values(cfg, seed, spec.stream, spec.steps[k].key, spec.steps[k].n, layers)
+            for k in range(k0, k0 + n_steps)]
+    t0 = time.perf_counter()
+    for j, k in enumerate(range(k0, k0 + n_steps)):
+        st, v = spec.steps[k], vals[j]
+        cache.append(st.seg, st.pos, st.unit, {l: v["k"][i] for i, l in enumerate(layers)},
+                     {l: v["v"][i] for i, l in enumerate(layers)})
+        for i, l in enumerate(layers):
+            cache.attention(l, v["q"][i], st.n)
+        if st.evict:
+            cache.evict(spec.budget, cfg.window)
+    dt = time.perf_counter() - t0
+    per_unit_all_layers = dt / n_units * (cfg.n_layers / sample_layers)
+    return {"value": 1.0 / per_unit_all_layers, "unit": "unit-steps/s", "cores": _threads_used(),
+            "kind": "oracle", "cpu_model": _cpu_model(), "host_cpus": os.cpu_count(),
+            "steps": [k0, k0 + n_steps],
+            "sample": f"{n_units} units ({n_steps} calls, steps {k0}..{k0 + n_steps - 1}, the first "
+                      f"timed units of the GPU leg) x {sample_layers} of {cfg.n_layers} layers, "
+                      f"append + attention + eviction, fp64 numpy, scaled to {cfg.n_layers} "
+                      f"layers; {dt:.1f} s of CPU work"}
+
+
 class Runner:
     """Shared plumbing: the library, a cache on torch's current stream, and
     per-kernel dispatch timing."""
@@ -639,6 +670,10 @@ def run_graph(args):
     graph = session(True)
     eager = session(False)
     ms_per_step = graph["total_ms"] / args.steps
+    base_line = None
+    if not args.no_cpu_baseline:
+        k = max(1, min(args.steps, args.cpu_sample_units))
+        base_line = cpu_baseline(cfg, spec, args.seed, first, k, args.cpu_sample_layers)
     return {
         "value": 1000.0 / ms_per_step,
         "ms_per_step": ms_per_step,
@@ -659,7 +694,7 @@ def run_graph(args):
         "peak_rows": graph["peak"], "end_rows": graph["end"],
         "same_session_end": graph["end"] == eager["end"] and graph["peak"] == eager["peak"],
         "roofline": None,
-        "cpu_baseline": None,
+        "cpu_baseline": base_line,
     }
 
 
@@ -944,6 +979,13 @@ def _cadence_session(args, kernel):
     kern_steps = [p0, p0 + args.profile_steps]
     steps_per_unit = sum(len(units[u]) for u in range(args.warmup, p0)) / max(1, args.steps)
     r.close()
+    base_line = None
+    if kernel is None and not args.no_cpu_baseline:
+        k0 = sum(len(units[u]) for u in range(args.warmup))
+        n_units = max(1, min(args.steps, 4))
+        n_steps = sum(len(units[u]) for u in range(args.warmup, args.warmup + n_units))
+        base_line = cpu_baseline_steps(cfg, args.seed, spec, k0, n_steps, n_units,
+                                       min(12, args.cpu_sample_layers))
     return {
         "value": 1000.0 * args.steps / total_ms,
         "ms_per_step": total_ms / args.steps,
@@ -962,7 +1004,7 @@ def _cadence_session(args, kernel):
         "kernels_us": kern,
         "kernels_us_steps": kern_steps,
         "timed_attention_calls": launches,
-        "cpu_baseline": None,
+        "cpu_baseline": base_line,
     }
 
 
@@ -1080,6 +1122,12 @@ def run_hour(args):
 
     ev = group(True)
     ctl = group(False)
+    base_line = None
+    if not args.no_cpu_baseline:
+        # one of the 16 streams (the oracle runs streams one at a time) on the evicting
+        # group's first timed units, 4 of 36 layers, scaled to all layers
+        base_line = cpu_baseline(cfg, specs[0], args.seed, t0, min(8, steps), 4)
+        base_line["unit"] = "stream unit-steps/s"
     return {
         "value": ev["stream_unit_steps_per_s"],
         "ms_per_step": ev["ms_per_step"],
@@ -1097,7 +1145,7 @@ def run_hour(args):
         "evict": ev,
         "control": ctl,
         "peak_reduction": 1.0 - ev["peak_rows_per_stream"] / ctl["peak_rows_per_stream"],
-        "cpu_baseline": None,
+        "cpu_baseline": base_line,
     }
 
 
