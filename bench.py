@@ -985,7 +985,7 @@ def _cadence_session(args, kernel):
         n_units = max(1, min(args.steps, 4))
         n_steps = sum(len(units[u]) for u in range(args.warmup, args.warmup + n_units))
         base_line = cpu_baseline_steps(cfg, args.seed, spec, k0, n_steps, n_units,
-                                       min(12, args.cpu_sample_layers))
+                                       args.cpu_sample_layers)
     return {
         "value": 1000.0 * args.steps / total_ms,
         "ms_per_step": total_ms / args.steps,
@@ -1125,8 +1125,8 @@ def run_hour(args):
     base_line = None
     if not args.no_cpu_baseline:
         # one of the 16 streams (the oracle runs streams one at a time) on the evicting
-        # group's first timed units, 4 of 36 layers, scaled to all layers
-        base_line = cpu_baseline(cfg, specs[0], args.seed, t0, min(8, steps), 4)
+        # group's first timed units, 16 of 36 layers, scaled to all layers
+        base_line = cpu_baseline(cfg, specs[0], args.seed, t0, min(8, steps), 16)
         base_line["unit"] = "stream unit-steps/s"
     return {
         "value": ev["stream_unit_steps_per_s"],
