@@ -164,7 +164,15 @@ typedef struct a2t_stream_info {
  * host bookkeeping of every stream (sized by unit_rows and max_step_rows) and
  * a small pinned-host staging area.
  * hip_stream: the hipStream_t to enqueue on (NULL = the default stream).
- * Pools hold L*S*Hkv*(unit_rows+kept_rows)*D elements for each of K and V. */
+ * Pools hold L*S*Hkv*(unit_rows+kept_rows)*D elements for each of K and V.
+ * Tuning read from the environment at creation (for tests and measurements;
+ * results stay within the attention tolerances whatever they are):
+ *   A2T_WS_MB       key-split workspace in MiB (default 256; a launch whose
+ *                   planned partials do not fit plans fewer splits)
+ *   A2T_TARGET_WGS  attention workgroups one launch spreads over (default:
+ *                   the device's CU count, one 8-wave workgroup per CU)
+ *   A2T_SPLITS      force this many key splits per stream (0 = planned)
+ *   A2T_FORCE_VALU  nonzero: the VALU attention kernel for bf16 caches too */
 int a2t_cache_create(const a2t_config* cfg, void* hip_stream, a2t_cache** out);
 
 /* Wait for the stream, then free everything the cache owns.  NULL is a no-op. */
