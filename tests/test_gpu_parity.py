@@ -214,6 +214,39 @@ def test_edge_streams_config1_heads(gpu, fused):
     assert ls.evictions > 5
 
 
+# step sizes that put the step's own rows on every kind of tile boundary: after a
+# 5-row prefix the cache reaches exactly 64 and 128 rows, a step of exactly one tile,
+# single decode rows, 63/65-row steps and 83-row units spanning up to three tiles
+TAIL_UNITS = [
+    [1] * 59, [1] * 62 + [2, 2], [4], [1] * 60 + [2, 3, 2],
+    [1] * 17 + [2] + [3] * 64 + [2], [1, 2], [1] * 61 + [2], [4], [4], [1] * 64,
+    [1] * 17 + [2] + [3] * 64 + [2], [1] * 40 + [2, 3, 3, 2], [1] * 64, [1] * 63, [4],
+    [1] * 65, [1] * 17 + [2, 3, 2], [1] * 30 + [2, 2],
+]
+
+
+@pytest.mark.parametrize("budget,window,unit_rows", [(10_000, 2, 1024), (300, 1, 400)])
+def test_fused_tail_split_layouts(gpu, budget, window, unit_rows):
+    """The fused path with planned key splits at the config-1 head shape, on steps
+    whose own rows start on, end on or span tile boundaries: a single-stream
+    launch gives the tiles holding the step's rows one-tile splits of their own,
+    and every step's attention, layout and stored K/V must still match the
+    oracle (without eviction, and with a 300-row budget and a wrapping ring)."""
+    cfg = CONFIGS[1]
+    spec = tiny_stream(TAIL_UNITS, prefix=5)
+    ls = Lockstep(cfg, 13, [spec], layers_checked=[0], n_layers=1, budgets=[budget],
+                  window=window, tol=BF16_TOL, unit_rows=unit_rows, kept_rows=400, max_step=84,
+                  fused=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    _report(ls, f"fused tail layouts B{budget}")
+    assert ls.steps_done == len(TAIL_UNITS) + 1
+    if budget < 10_000:
+        assert ls.evictions > 3
+
+
 def test_short_cache_single_partial_tile(gpu):
     # R < 64 keys: one partial tile, masked tail
     cfg = CONFIGS[0]
