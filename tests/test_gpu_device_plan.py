@@ -218,6 +218,45 @@ def test_device_planned_rule_variants_config0(gpu, rule, n_sink, budgets):
     assert run.evictions > 40
 
 
+@pytest.mark.parametrize("case", range(12))
+def test_device_planned_random_shapes(gpu, case):
+    """Seeded random shapes through the device-planned calls: head counts and
+    groups, head dims, up to five streams of one length with their own budgets,
+    unit sizes, windows, rules and layer counts, every step checked in full."""
+    import dataclasses
+    from tests.test_gpu_random_shapes import HEADS
+    rng = np.random.default_rng(2000 + case)
+    hq, hkv = HEADS[int(rng.integers(len(HEADS)))]
+    acoustic, cap = int(rng.integers(2, 41)), int(rng.choice([4, 16, 64]))
+    cfg = dataclasses.replace(CONFIGS[0], index=200 + case, n_q_heads=hq, n_kv_heads=hkv,
+                              head_dim=int(rng.choice([64, 128])), dtype="bf16",
+                              n_streams=int(rng.choice([1, 2, 3, 5])),
+                              units=int(rng.integers(15, 41)), acoustic_rows=acoustic,
+                              text_mean=float(rng.uniform(0.3, 6.0)), text_cap=cap,
+                              window=int(rng.choice([0, 1, 2, 5])))
+    rule = [None, "row", "sink_recent"][int(rng.integers(3))]
+    n_sink = int(rng.integers(0, 6)) if rule == "sink_recent" else 0
+    n_layers = int(rng.choice([1, 2, 3]))
+    specs = make_workload(cfg, seed=cfg.index).streams
+    unit = acoustic + 2 + cap
+    budgets = [max(n_sink, int(rng.integers(0, 10 * unit))) for _ in specs]
+    run = DevRun(cfg, cfg.index, specs, budgets, cfg.window, sorted({0, n_layers - 1}), n_layers,
+                 rule=rule, n_sink=n_sink, **_bounds(specs))
+    import paper_2609_31224_amd as a2t
+    try:
+        a2t.a2t_dev_begin(run.cache)
+        for t in range(len(specs[0].steps)):
+            run.fill(t)
+            run.issue()
+            run.check(full=True)
+        a2t.a2t_dev_end(run.cache)
+    finally:
+        run.close()
+    print(f"[device random {case}] heads {hq}/{hkv} D{cfg.head_dim} streams {len(specs)} "
+          f"B {budgets} W {cfg.window} rule={rule or 'unit'} sinks {n_sink} L={n_layers}: "
+          f"evictions {run.evictions} max err {run.max_err:.2e}", flush=True)
+
+
 def test_device_planned_sink_rule_errors(gpu):
     """A budget below the sink count is refused on the device for that stream
     only (A2T_ERR_INVALID from a2t_dev_end, nothing evicted); the other stream
