@@ -400,12 +400,13 @@ struct WsChoice {
 int64_t planned_partials(a2t_cache* c, int n, const int32_t* ids, const int32_t* n_q,
                          const int32_t* extra, int64_t ws_limit) {
     const int G = c->cfg.n_q_heads / c->cfg.n_kv_heads;
+    const int64_t rf = partial_row_floats(c->cfg.head_dim, c->cfg.dtype == A2T_F32 || c->force_valu);
     int tiles[kMaxDesc], nsplit[kMaxDesc];
     int64_t floats[kMaxDesc];
     for (int i = 0; i < n; ++i) {
         const int64_t R = c->ss[ids[i]].resident() + (extra ? extra[i] : 0);
         tiles[i] = (int)std::max<int64_t>(1, (R + kTileKeys - 1) / kTileKeys);
-        floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
+        floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * rf;
     }
     plan_splits(c, n, tiles, floats, nsplit, ws_limit);
     int64_t total = 0;
@@ -424,13 +425,18 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     b.count = n;
     b.layer = layer;
     const int G = c->cfg.n_q_heads / c->cfg.n_kv_heads;
+    // bf16 caches use the MFMA kernel for decode too: with one query row per
+    // stream it is still bound by streaming the resident K/V, and its staged
+    // tile pipeline keeps more bytes in flight than the VALU kernel.
+    const bool valu = c->cfg.dtype == A2T_F32 || c->force_valu;
+    const int64_t rf = partial_row_floats(c->cfg.head_dim, valu);
     int max_rows = 0, tiles[kMaxDesc], nsplit[kMaxDesc];
     int64_t floats[kMaxDesc];
     for (int i = 0; i < n; ++i) {
         const StreamState& s = c->ss[ids[i]];
         tiles[i] = std::max(1, (s.resident() + kTileKeys - 1) / kTileKeys);
         max_rows = std::max(max_rows, n_q[i]);
-        floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * (c->cfg.head_dim + 2);
+        floats[i] = (int64_t)c->cfg.n_kv_heads * G * n_q[i] * rf;
     }
     plan_splits(c, n, tiles, floats, nsplit, wsc ? INT64_MAX : c->dev.ws_floats);
     // descriptors in order of falling tiles per split: the dispatcher starts the
@@ -461,7 +467,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         d.n_new = in_row0 ? s.step_rows : 0;
         d.in_row0 = in_row0 ? in_row0[i] : 0;
         d.ws_off = off;
-        if (d.splits > 1) off += (int64_t)d.splits * c->cfg.n_kv_heads * G * d.n_q * (c->cfg.head_dim + 2);
+        if (d.splits > 1) off += (int64_t)d.splits * c->cfg.n_kv_heads * G * d.n_q * rf;
     }
     // a fused step's own rows: when the launch's workgroups (with one more split
     // per tile holding them) still fit one round over the CUs, those tiles get
@@ -488,7 +494,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
                 }
             }
             wgs += (int64_t)ns[k] * Hkv;
-            if (ns[k] > 1) ws += (int64_t)ns[k] * Hkv * G * d.n_q * (c->cfg.head_dim + 2);
+            if (ns[k] > 1) ws += (int64_t)ns[k] * Hkv * G * d.n_q * rf;
         }
         if (any && wgs <= c->target_wgs && ws <= c->dev.ws_floats) {
             int64_t o2 = 0;
@@ -496,7 +502,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
                 AttnDesc& d = b.d[k];
                 d.splits = ns[k], d.tile_q = tq[k], d.tile_r = tr[k];
                 d.ws_off = o2;
-                if (d.splits > 1) o2 += (int64_t)d.splits * Hkv * G * d.n_q * (c->cfg.head_dim + 2);
+                if (d.splits > 1) o2 += (int64_t)d.splits * Hkv * G * d.n_q * rf;
                 splits = std::max(splits, (int)d.splits);
             }
             off = o2;
@@ -504,10 +510,6 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     }
     b.max_splits = splits;
     b.max_rows = max_rows;
-    // bf16 caches use the MFMA kernel for decode too: with one query row per
-    // stream it is still bound by streaming the resident K/V, and its staged
-    // tile pipeline keeps more bytes in flight than the VALU kernel.
-    const bool valu = c->cfg.dtype == A2T_F32 || c->force_valu;
     hipError_t e;
     if (wsc) {
         // the caller checked the partials against the fixed array before any state changed
@@ -518,7 +520,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         const KTimer none{};
         e = valu ? launch_attn_valu(st, b, q, o, c->stream, none)
                  : launch_attn_tile(st, b, q, o, k_in, v_in, c->stream, none);
-        if (e == hipSuccess && splits > 1) e = launch_attn_merge(st, b, o, c->stream, none);
+        if (e == hipSuccess && splits > 1) e = launch_attn_merge(st, b, o, c->stream, none, !valu);
         return e == hipSuccess ? A2T_OK : hip_fail(c);
     }
     {
@@ -529,7 +531,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
     if (e != hipSuccess) return hip_fail(c);
     if (splits > 1) {
         ProfScope ps(c, "attn_merge");
-        if (launch_attn_merge(c->dev, b, o, c->stream, ps.kt()) != hipSuccess) return hip_fail(c);
+        if (launch_attn_merge(c->dev, b, o, c->stream, ps.kt(), !valu) != hipSuccess) return hip_fail(c);
     }
     return A2T_OK;
 }

@@ -214,8 +214,12 @@ hipError_t launch_attn_tile(const DevState& st, const AttnBatch& b, const void* 
 // VALU attention, one (row, kv head) per workgroup column (fp32 caches, decode).
 hipError_t launch_attn_valu(const DevState& st, const AttnBatch& b, const void* q, void* o,
                             hipStream_t stream, const KTimer& kt);
+// h16: the partials come from the MFMA kernel (fp16 O rows), else from the VALU kernel (fp32)
 hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o,
-                             hipStream_t stream, const KTimer& kt);
+                             hipStream_t stream, const KTimer& kt, bool h16);
+// Floats of key-split partials per query row and head: O (fp16 from the MFMA kernel,
+// fp32 from the VALU kernel) and the fp32 (max, sum) pair.
+inline int64_t partial_row_floats(int head_dim, bool valu) { return (valu ? head_dim : head_dim / 2) + 2; }
 hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream,
                         const KTimer& kt);
 

@@ -37,6 +37,7 @@ constexpr uint8_t kSegDelim = 2;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 struct bf16_t {
     uint16_t bits;
@@ -334,6 +335,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 // max / sum over the four lanes l, l^16, l^32, l^48 (the lanes holding one
 // query column of a 16x16 accumulator), with the gfx950 row-swap permutes
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
+}
 __device__ __forceinline__ float quad_max(float x) {
     const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
@@ -862,6 +867,42 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
         }
 
         if (active) lrun = quad_sum(lrun);
+        if (active && d.splits > 1) {
+            // key-split partial: O / sum in fp16 (a row with no visible key in this
+            // split stores zeros, which its zero weight in the merge ignores) and fp32
+            // (max, sum).  A lane holds dims 16 db + 4 lg .. + 3 of its row; lanes
+            // lg and lg ^ 1 swap halves of a block pair so that each lane stores 8
+            // adjacent dims (16 bytes): even lg the pair's first block, odd lg its
+            // second.  Every lane of the wave takes part in the swaps.  Split
+            // partials are read once, by the merge launch: non-temporal stores send
+            // them on to memory now instead of leaving dirty L2 lines for the
+            // end-of-kernel write-back.
+            const float inv = lrun > 0.f ? 1.f / lrun : 0.f;
+            u32x4 ho[DB / 2];
+#pragma unroll
+            for (int j = 0; j < DB / 2; ++j) {
+                const f32x4 a0 = acc[2 * j], a1 = acc[2 * j + 1];
+                const uint32_t h00 = pack_f16x2(a0[0] * inv, a0[1] * inv), h01 = pack_f16x2(a0[2] * inv, a0[3] * inv);
+                const uint32_t h10 = pack_f16x2(a1[0] * inv, a1[1] * inv), h11 = pack_f16x2(a1[2] * inv, a1[3] * inv);
+                // odd rows (16 lanes) of the first operand trade with even rows of the second
+                const auto s0 = __builtin_amdgcn_permlane16_swap(h00, h10, false, false);
+                const auto s1 = __builtin_amdgcn_permlane16_swap(h01, h11, false, false);
+                ho[j] = (lg & 1) ? u32x4{s0[0], s1[0], h10, h11} : u32x4{h00, h01, s0[1], s1[1]};
+            }
+            if (mq < M) {
+                float* po = st.ws + d.ws_off;
+                _Float16* prow = reinterpret_cast<_Float16*>(po) + (((int64_t)sp * st.Hkv + g) * M + mq) * D;
+#pragma unroll
+                for (int j = 0; j < DB / 2; ++j)
+                    __builtin_nontemporal_store(ho[j], reinterpret_cast<u32x4*>(prow + 32 * j + 16 * (lg & 1) + 4 * (lg & ~1)));
+                if (lg == 0) {
+                    float* pml = po + (int64_t)d.splits * st.Hkv * M * (D / 2);
+                    float* mp = pml + (((int64_t)sp * st.Hkv + g) * M + mq) * 2;
+                    __builtin_nontemporal_store(mrun, mp);
+                    __builtin_nontemporal_store(lrun, mp + 1);
+                }
+            }
+        }
         if (active && mq < M) {
             const int i = mq / G, hh = mq - i * G;
             if (d.splits == 1) {
@@ -873,21 +914,6 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                     *reinterpret_cast<uint2*>(op + db * 16 + 4 * lg) =
                         make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
                 }
-            } else {
-                // split partials are read once, by the merge launch: non-temporal
-                // stores send them on to memory now instead of leaving dirty L2
-                // lines for the end-of-kernel write-back
-                float* po = st.ws + d.ws_off;
-                float* prow = po + (((int64_t)sp * st.Hkv + g) * M + mq) * D;
-#pragma unroll
-                for (int db = 0; db < DB; ++db)
-                    __builtin_nontemporal_store(acc[db], reinterpret_cast<f32x4*>(prow + db * 16 + 4 * lg));
-                if (lg == 0) {
-                    float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
-                    float* mp = pml + (((int64_t)sp * st.Hkv + g) * M + mq) * 2;
-                    __builtin_nontemporal_store(mrun, mp);
-                    __builtin_nontemporal_store(lrun, mp + 1);
-                }
             }
         }
         if (qg0 + QPP < M) __syncthreads();  // the stages are reused by the next pass over the keys
@@ -896,48 +922,56 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
 
 // ----------------------------------------------------------------- attn_merge
 // grid (row groups x kv heads, stream).  A workgroup combines the key-split
-// partials of kMergeRows query rows: each thread owns 4 output elements of one
-// row and the splits s = sg, sg + NSG, ... of its split group sg (NSG = 2 at
-// head dim 128), read B at a time with all loads of a batch in flight
-// together (the launch picks B = 12 when more than 16 splits would take two
-// rounds of 8, else 8, which holds fewer registers).  The split groups'
-// running (max, sum, O) then combine in LDS in group order.  Spreading a row's splits over NSG threads spreads the partials
-// over more workgroups than one thread per four outputs would: the partials
-// come from memory and a CU streams only so many bytes per microsecond.  The
-// order of every sum is fixed, so the result is deterministic.
+// partials of kMergeRows query rows: each thread owns 8 output elements of one
+// row (the MFMA kernel's fp16 partials; 4 from the VALU kernel's fp32 ones, one
+// 16-byte load per split either way) and the splits s = sg, sg + NSG, ... of
+// its split group sg (NSG = 4 at head dim 128 with fp16 partials, 2 with fp32),
+// read B at a time with all loads of a batch in flight together (the launch
+// picks B = 12 when a thread would otherwise take two rounds of 8, else 8,
+// which holds fewer registers).  The split groups' running (max, sum, O) then
+// combine in LDS in group order.  Spreading a row's splits over NSG threads
+// spreads the partials over more workgroups than one thread per row would: the
+// partials come from memory and a CU streams only so many bytes per
+// microsecond.  The order of every sum is fixed, so the result is deterministic.
 // One row group (kMergeRows query rows of KV head g) of the merge; every thread
 // of the workgroup calls it (one barrier inside).
-template <typename T, int B>
+template <typename T, int B, bool H16>
 __device__ __forceinline__ void merge_row_group(const DevState& st, const AttnDesc& d, T* o, int g,
                                                 int rg, float4* s_o, float2* s_ml) {
-    constexpr int MR = kMergeRows;
+    // EPT output elements per thread: 4 from fp32 partials (one 16-byte load per
+    // split), 8 from fp16 partials (also one 16-byte load)
+    constexpr int MR = kMergeRows, EPT = H16 ? 8 : 4;
     const int G = st.G, M = G * d.n_q, D = st.D;
-    const int tpr = D / 4;          // threads per query row
+    const int tpr = D / EPT;        // threads per query row
     const int tsg = MR * tpr;       // threads per split group
     const int nsg = 256 / tsg;      // split groups
     const int sg = threadIdx.x / tsg, r = threadIdx.x - sg * tsg;
-    const int rr = r / tpr, d4 = (r - rr * tpr) * 4;
+    const int rr = r / tpr, de = (r - rr * tpr) * EPT;
     const int mq = rg * MR + rr;
     const bool live = mq < M;
     const int mqc = live ? mq : M - 1;
+    // floats per stored O row: D (fp32) or D / 2 (fp16); (max, sum) pairs after the O rows
+    const int ow = H16 ? D / 2 : D;
     const float* po = st.ws + d.ws_off;
-    const float* pml = po + (int64_t)d.splits * st.Hkv * M * D;
-    const int64_t ostride = (int64_t)st.Hkv * M * D, mstride = (int64_t)st.Hkv * M * 2;
-    const float* orow = po + ((int64_t)g * M + mqc) * D + d4;
+    const float* pml = po + (int64_t)d.splits * st.Hkv * M * ow;
+    const int64_t ostride = (int64_t)st.Hkv * M * ow, mstride = (int64_t)st.Hkv * M * 2;
+    const float* orow = po + ((int64_t)g * M + mqc) * ow + (H16 ? de / 2 : de);
     const float* mrow = pml + ((int64_t)g * M + mqc) * 2;
-    float mx = -INFINITY, L = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
+    float mx = -INFINITY, L = 0.f, O[EPT];
+#pragma unroll
+    for (int e2 = 0; e2 < EPT; ++e2) O[e2] = 0.f;
     for (int s0 = sg; s0 < d.splits; s0 += B * nsg) {
         float2 ml[B];
-        float4 ov[B];
+        u32x4 ov[B];
 #pragma unroll
         for (int j = 0; j < B; ++j) {
             const int s = s0 + j * nsg;
             if (s < d.splits) {
                 ml[j] = *reinterpret_cast<const float2*>(mrow + s * mstride);
-                ov[j] = *reinterpret_cast<const float4*>(orow + s * ostride);
+                ov[j] = *reinterpret_cast<const u32x4*>(orow + s * ostride);
             } else {
                 ml[j] = make_float2(-INFINITY, 0.f);
-                ov[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+                ov[j] = u32x4{0u, 0u, 0u, 0u};
             }
         }
         float bm = mx;
@@ -947,25 +981,35 @@ __device__ __forceinline__ void merge_row_group(const DevState& st, const AttnDe
         const float c = (mx == -INFINITY) ? 0.f : exp2f(mx - bm);
         L *= c;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) O[e] *= c;
+        for (int e2 = 0; e2 < EPT; ++e2) O[e2] *= c;
 #pragma unroll
         for (int j = 0; j < B; ++j) {
-            const float w = (ml[j].x == -INFINITY) ? 0.f : exp2f(ml[j].x - bm);
-            L += w * ml[j].y;
-            O[0] += w * ov[j].x;
-            O[1] += w * ov[j].y;
-            O[2] += w * ov[j].z;
-            O[3] += w * ov[j].w;
+            // fp32 partials hold O unnormalised (weight exp2(m - bm)); fp16 partials hold
+            // O / sum (weight exp2(m - bm) * sum), which keeps them within fp16 range
+            const float w0 = (ml[j].x == -INFINITY) ? 0.f : exp2f(ml[j].x - bm);
+            L += w0 * ml[j].y;
+            if constexpr (H16) {
+                const float w = w0 * ml[j].y;
+                const f16x8 h = __builtin_bit_cast(f16x8, ov[j]);
+#pragma unroll
+                for (int e2 = 0; e2 < 8; ++e2) O[e2] += w * (float)h[e2];
+            } else {
+#pragma unroll
+                for (int e2 = 0; e2 < 4; ++e2) O[e2] += w0 * __uint_as_float(ov[j][e2]);
+            }
         }
         mx = bm;
     }
     s_o[threadIdx.x] = make_float4(O[0], O[1], O[2], O[3]);
+    if constexpr (H16) s_o[256 + threadIdx.x] = make_float4(O[4], O[5], O[6], O[7]);
     s_ml[threadIdx.x] = make_float2(mx, L);
     __syncthreads();
     if (sg != 0 || !live) return;
     float bm = -INFINITY;
     for (int k = 0; k < nsg; ++k) bm = fmaxf(bm, s_ml[k * tsg + r].x);
-    float Lt = 0.f, Ot[4] = {0.f, 0.f, 0.f, 0.f};
+    float Lt = 0.f, Ot[EPT];
+#pragma unroll
+    for (int e2 = 0; e2 < EPT; ++e2) Ot[e2] = 0.f;
     for (int k = 0; k < nsg; ++k) {
         const float2 ml = s_ml[k * tsg + r];
         if (ml.x == -INFINITY) continue;
@@ -976,17 +1020,25 @@ __device__ __forceinline__ void merge_row_group(const DevState& st, const AttnDe
         Ot[1] += w * ov.y;
         Ot[2] += w * ov.z;
         Ot[3] += w * ov.w;
+        if constexpr (H16) {
+            const float4 ov2 = s_o[256 + k * tsg + r];
+            Ot[4] += w * ov2.x;
+            Ot[5] += w * ov2.y;
+            Ot[6] += w * ov2.z;
+            Ot[7] += w * ov2.w;
+        }
     }
     const float inv = 1.f / Lt;
     const int i = mq / G, hh = mq - i * G;
-    T* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D + d4;
+    T* op = o + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D + de;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) Elt<T>::store(op + e, Ot[e] * inv);
+    for (int e2 = 0; e2 < EPT; ++e2) Elt<T>::store(op + e2, Ot[e2] * inv);
 }
 
-template <typename T, int B, class BT>
+// H16: the partials of the MFMA attention kernel (fp16 O rows); else fp32 (VALU kernel)
+template <typename T, int B, class BT, bool H16 = false>
 __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
-    __shared__ float4 s_o[256];
+    __shared__ float4 s_o[H16 ? 512 : 256];
     __shared__ float2 s_ml[256];
     const AttnDesc d = b.d[blockIdx.z];
     if (d.splits <= 1) return;
@@ -997,7 +1049,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o
     const int g = blockIdx.x % st.Hkv, groups = gridDim.x / st.Hkv;
     const int M = st.G * d.n_q;
     for (int rg = blockIdx.x / st.Hkv; rg * kMergeRows < M; rg += groups) {
-        merge_row_group<T, B>(st, d, o, g, rg, s_o, s_ml);
+        merge_row_group<T, B, H16>(st, d, o, g, rg, s_o, s_ml);
         __syncthreads();   // s_o / s_ml are reused by the next row group
     }
 }
@@ -1172,7 +1224,7 @@ __global__ __launch_bounds__(64) void dev_open_kernel(DevState st, DevStepArgs a
     }
     __syncthreads();
     if (i != 0) return;
-    const int64_t row_floats = st.D + 2;   // split partials of one query row and head
+    const int64_t row_floats = st.D / 2 + 2;   // split partials of one query row and head (fp16 O)
     int max_tiles = 1;
     for (int k = 0; k < a.count; ++k)
         if (s_n[k]) max_tiles = max(max_tiles, (s_R[k] + kTileKeys - 1) / kTileKeys);
@@ -1351,9 +1403,9 @@ __global__ __launch_bounds__(256) void dev_evict_plan_kernel(DevState st, DevSte
 
 // ------------------------------------------------------------- fixed workspace
 // Key-split partials of a2t_append_attn_noalloc: one launch's partials (every
-// split's unnormalised O rows, then their (max, sum) pairs) in a fixed device
-// array instead of a cache's workspace.  16 MiB holds the partials of a
-// 22-split launch over 22 query rows x 32 heads x head dim 128 twice over.
+// split's O rows, then their (max, sum) pairs) in a fixed device array instead
+// of a cache's workspace.  16 MiB holds the fp16 partials of a 22-split launch
+// over 22 query rows x 32 heads x head dim 128 four times over.
 // Every call on a device shares that device's copy; each attention launch
 // writes every partial its merge reads, so nothing needs clearing between calls.
 constexpr int64_t kScratchFloats = int64_t(4) << 20;
@@ -1485,15 +1537,22 @@ hipError_t launch_attn_valu(const DevState& st, const AttnBatch& b, const void* 
 }
 
 hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hipStream_t stream,
-                             const KTimer& kt) {
+                             const KTimer& kt, bool h16) {
     const int G = st.Hq / st.Hkv;
     if (st.D / 4 * kMergeRows > 256) return hipErrorInvalidValue;
+    if (h16 && st.dtype == 0) return hipErrorInvalidValue;   // fp16 partials come from bf16 caches
     const dim3 grid((G * b.max_rows + kMergeRows - 1) / kMergeRows * st.Hkv, 1, b.count);
-    const int nsg = 256 / (kMergeRows * st.D / 4);                // split groups per workgroup
+    const int nsg = 256 / (kMergeRows * st.D / (h16 ? 8 : 4));    // split groups per workgroup
     const bool wide = (b.max_splits + nsg - 1) / nsg > 8;          // more than one round of 8
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
-        if (st.dtype == 0 && wide)
+        if (h16 && wide)
+            A2T_DISPATCH((attn_merge_kernel<bf16_t, 12, B, true>), grid, dim3(256), stream, kt, st, bb,
+                         static_cast<bf16_t*>(o));
+        else if (h16)
+            A2T_DISPATCH((attn_merge_kernel<bf16_t, 8, B, true>), grid, dim3(256), stream, kt, st, bb,
+                         static_cast<bf16_t*>(o));
+        else if (st.dtype == 0 && wide)
             A2T_DISPATCH((attn_merge_kernel<float, 12, B>), grid, dim3(256), stream, kt, st, bb,
                          static_cast<float*>(o));
         else if (st.dtype == 0)
@@ -1555,12 +1614,12 @@ hipError_t launch_attn_merge_dev(const DevState& st, const DevPlan* plan, int co
     // at most kDevMergeGroups row groups per head; the kernel strides over the rest
     const int groups = std::min((G * st.max_step_rows + kMergeRows - 1) / kMergeRows, kDevMergeGroups);
     const dim3 grid(groups * st.Hkv, 1, count);
-    const int nsg = 256 / (kMergeRows * st.D / 4);
+    const int nsg = 256 / (kMergeRows * st.D / 8);   // fp16 partials of the MFMA kernel
     if ((max_splits + nsg - 1) / nsg > 8)
-        hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 12, DevBatch<AttnDesc>>), grid, dim3(256), 0,
+        hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 12, DevBatch<AttnDesc>, true>), grid, dim3(256), 0,
                            stream, st, b, static_cast<bf16_t*>(o));
     else
-        hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 8, DevBatch<AttnDesc>>), grid, dim3(256), 0,
+        hipLaunchKernelGGL((attn_merge_kernel<bf16_t, 8, DevBatch<AttnDesc>, true>), grid, dim3(256), 0,
                            stream, st, b, static_cast<bf16_t*>(o));
     return hipGetLastError();
 }
