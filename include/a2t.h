@@ -213,6 +213,12 @@ int a2t_append(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* st
  *   q     device [sum n_q][Hq][D], pre-rotation.
  *   o     device [sum n_q][Hq][D], written with softmax(scale q.K^T) V over the
  *         resident rows of `layer` up to each query's own row.
+ * Scores, the softmax and the output sums are fp32.  When a launch splits a
+ * stream's keys over several workgroups, each split's output rows of a bf16
+ * cache are held in fp16 until they are combined (normalised by the split's
+ * own sum, so each value lies within the range of the V entries): bf16 V
+ * entries must stay within fp16's range (|v| <= 65504).  fp32 caches keep
+ * fp32 split outputs.
  * The layer must have appended the current step.  Errors: INVALID, STATE. */
 int a2t_chunk_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* stream_ids,
                    const int32_t* n_q, const void* q, void* o);
@@ -236,8 +242,10 @@ int a2t_append_attn(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_
  * on a cache created with A2T_FLAG_NO_WORKSPACE.  Splits are planned as
  * a2t_append_attn plans them without a workspace limit; a call whose launch
  * would write more than 16 MiB of partials (4,194,304 floats; a stream's
- * partials are splits x n_q x n_q_heads x (head_dim + 2) floats, about 8 MiB
- * for 22 query rows x 32 heads x head dim 128 at ~4,100 resident rows) is
+ * partials are splits x n_q x n_q_heads x (head_dim / 2 + 2) floats for a bf16
+ * cache, fp16 output rows with an fp32 maximum and sum, and x (head_dim + 2)
+ * for an fp32 cache: about 4 MiB for 22 query rows x 32 heads x head dim 128
+ * at ~4,100 resident rows, 23 splits) is
  * rejected with A2T_ERR_CAPACITY before anything changes.  Every call on a GPU
  * shares that GPU's array: calls that overlap on one GPU (two caches on
  * different streams, or two host threads) race and must be serialised by the
