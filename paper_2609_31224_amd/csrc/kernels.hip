@@ -785,6 +785,16 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
                         sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[s][kb]),
                                                                            qop[s], sacc[kb], 0, 0, 0);
             }
+            // the V operands of keys 0..31 are requested before the softmax, those
+            // of keys 32..63 under the products of the first half: the LDS reads'
+            // latency overlaps the exponentials and the MFMAs
+            const uint32_t vb = lds_addr(&buf.v[0]);
+            uint2 lo0[DB], hi0[DB];
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                lo0[db] = lds_tr16_issue<0>(vb + vtr_off[db]);
+                hi0[db] = lds_tr16_issue<16 * D * 2>(vb + vtr_off[db]);
+            }
             if (kbase + kTileKeys - 1 > vis0) {
 #pragma unroll
                 for (int kb = 0; kb < 4; ++kb)
@@ -823,26 +833,30 @@ __global__ __launch_bounds__(kMfmaThreads) void attn_tile_kernel(DevState st, BT
             // k-slots 8*lg+0..3 hold keys 32c + 4lg + 0..3 and 8*lg+4..7 keys
             // 32c+16+4lg+0..3; this lane's transposed reads start at row 32c+4lg+(l16>>2)
             // (+16) and dims 16db + 4(l16&3) (the row offsets are immediates)
-            const uint32_t vb = lds_addr(&buf.v[0]);
-            auto pv_step = [&](auto cc) {
-                constexpr int c = decltype(cc)::value;
-                const bf16x8 pop = __builtin_bit_cast(
-                    bf16x8, make_uint4(pk[2 * c][0], pk[2 * c][1], pk[2 * c + 1][0], pk[2 * c + 1][1]));
-                uint2 lo[DB], hi[DB];
+            lds_wait_all(lo0, hi0);
+            uint2 lo1[DB], hi1[DB];
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                lo1[db] = lds_tr16_issue<32 * D * 2>(vb + vtr_off[db]);
+                hi1[db] = lds_tr16_issue<48 * D * 2>(vb + vtr_off[db]);
+            }
+            {
+                const bf16x8 pop = __builtin_bit_cast(bf16x8, make_uint4(pk[0][0], pk[0][1], pk[1][0], pk[1][1]));
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
-                    lo[db] = lds_tr16_issue<c * 32 * D * 2>(vb + vtr_off[db]);
-                    hi[db] = lds_tr16_issue<(c * 32 + 16) * D * 2>(vb + vtr_off[db]);
-                }
-                lds_wait_all(lo, hi);
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(lo[db].x, lo[db].y, hi[db].x, hi[db].y));
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(lo0[db].x, lo0[db].y, hi0[db].x, hi0[db].y));
                     acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pop, acc[db], 0, 0, 0);
                 }
-            };
-            pv_step(std::integral_constant<int, 0>{});
-            pv_step(std::integral_constant<int, 1>{});
+            }
+            lds_wait_all(lo1, hi1);
+            {
+                const bf16x8 pop = __builtin_bit_cast(bf16x8, make_uint4(pk[2][0], pk[2][1], pk[3][0], pk[3][1]));
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(lo1[db].x, lo1[db].y, hi1[db].x, hi1[db].y));
+                    acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pop, acc[db], 0, 0, 0);
+                }
+            }
         };
 
         // one tile: wait for its DMA (only later tiles' DMA may stay in flight),
