@@ -41,18 +41,43 @@ def draw_case(i):
                 n_sink=int(rng.integers(0, 6)), n_layers=int(rng.choice([1, 1, 2, 3])))
 
 
+def _env(name, value):
+    """Set (or, for None, clear) an environment variable; returns the old value."""
+    old = os.environ.get(name)
+    if value is None:
+        os.environ.pop(name, None)
+    else:
+        os.environ[name] = value
+    return old
+
+
 @pytest.mark.parametrize("case", range(48))
 def test_random_shape(gpu, case):
+    _run_case(draw_case(case), f"random {case}")
+
+
+@pytest.mark.parametrize("case", range(100, 106))
+def test_random_shape_forced_valu(gpu, case):
+    """bf16 caches on the VALU kernel (A2T_FORCE_VALU, read at cache creation):
+    its fp32 key-split partials and the merge that reads them, unfused calls."""
     c = draw_case(case)
+    c["cfg"] = dataclasses.replace(c["cfg"], dtype="bf16")
+    c["fused"] = False
+    old = _env("A2T_FORCE_VALU", "1")
+    try:
+        _run_case(c, f"forced VALU {case}")
+    finally:
+        _env("A2T_FORCE_VALU", old)
+
+
+def _run_case(c, label):
     cfg = c["cfg"]
     specs = make_workload(cfg, seed=cfg.index).streams
     budgets = [s.budget for s in specs]
     if c["rule"] == "sink_recent":
         budgets = [max(b, c["n_sink"]) for b in budgets]
     layers = sorted({0, c["n_layers"] - 1})
-    old = os.environ.get("A2T_SPLITS")
-    if c["splits"]:
-        os.environ["A2T_SPLITS"] = c["splits"]
+    old = _env("A2T_SPLITS", c["splits"] or os.environ.get("A2T_SPLITS"))
     try:
         ls = Lockstep(cfg, cfg.index, specs, layers_checked=layers, n_layers=c["n_layers"],
                       budgets=budgets, window=cfg.window,
@@ -66,11 +91,8 @@ def test_random_shape(gpu, case):
         finally:
             ls.close()
     finally:
-        if old is None:
-            os.environ.pop("A2T_SPLITS", None)
-        else:
-            os.environ["A2T_SPLITS"] = old
-    print(f"[random {case}] heads {cfg.n_q_heads}/{cfg.n_kv_heads} D{cfg.head_dim} {cfg.dtype} "
+        _env("A2T_SPLITS", old)
+    print(f"[{label}] heads {cfg.n_q_heads}/{cfg.n_kv_heads} D{cfg.head_dim} {cfg.dtype} "
           f"streams {len(specs)} units<= {cfg.units} rows/unit<= {cfg.max_unit_rows} "
           f"B {budgets} W {cfg.window} fused={c['fused']} splits={c['splits'] or 'planned'} "
           f"rule={c['rule'] or 'unit'} L={c['n_layers']}: steps {ls.steps_done} evictions "
