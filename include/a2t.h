@@ -389,6 +389,13 @@ int a2t_dev_evict_rule(a2t_cache* c, const int32_t* budget, int32_t window, int3
 /* Bookkeeping of one stream (host state, no synchronisation). */
 int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out);
 
+/* A stream's resident row count R and its peak (Sec. 3.3: the budget is checked
+ * against R after each unit; the peak is the largest R right after an append).
+ * n, peak: host, either may be NULL.  Host bookkeeping only, no device access.
+ * Errors: INVALID (stream out of range), STATE (device-planned steps hold the
+ * state: a2t_dev_end first). */
+int a2t_resident(const a2t_cache* c, int32_t stream, int32_t* n, int32_t* peak);
+
 /* Copy one stream's layout to host, in cache order (synchronises).
  * pos, seg, unit: host [resident] (any may be NULL).  The values are read from
  * the device metadata, not from the host state. */

@@ -40,7 +40,7 @@ EXPORTED = (
     "a2t_chunk_attn", "a2t_append_attn", "a2t_append_attn_noalloc", "a2t_decode_attn",
     "a2t_evict", "a2t_evict_rule", "a2t_dev_begin", "a2t_dev_end", "a2t_dev_open",
     "a2t_dev_append_attn", "a2t_dev_evict", "a2t_dev_evict_rule",
-    "a2t_stream_info_get",
+    "a2t_stream_info_get", "a2t_resident",
     "a2t_read_layout", "a2t_read_last_evict", "a2t_read_kv", "a2t_sync",
     "a2t_profile_enable", "a2t_kernel_time", "a2t_profile_reserve", "a2t_status_str",
     "a2t_abi_version", "a2t_distill_create", "a2t_distill_destroy", "a2t_distill_loss",
@@ -103,6 +103,7 @@ def _load():
         "a2t_dev_evict": (C.c_int, [VP, VP, I32, VP, VP]),
         "a2t_dev_evict_rule": (C.c_int, [VP, VP, I32, I32, I32, VP, VP]),
         "a2t_stream_info_get": (C.c_int, [VP, I32, P(a2t_stream_info)]),
+        "a2t_resident": (C.c_int, [VP, I32, P(C.c_int32), P(C.c_int32)]),
         "a2t_read_layout": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
         "a2t_read_last_evict": (C.c_int, [VP, I32, P(I32), P(C.c_uint8), P(I32)]),
         "a2t_read_kv": (C.c_int, [VP, I32, I32, VP, VP]),
@@ -355,6 +356,13 @@ def a2t_stream_info_get(c: Cache, stream: int) -> dict:
     info = a2t_stream_info()
     _check(_lib.a2t_stream_info_get(c.ptr, stream, C.byref(info)), "a2t_stream_info_get")
     return {name: getattr(info, name) for name, _ in a2t_stream_info._fields_}
+
+
+def a2t_resident(c: Cache, stream: int) -> tuple:
+    """(resident rows R, peak R) of one stream."""
+    n, peak = C.c_int32(), C.c_int32()
+    _check(_lib.a2t_resident(c.ptr, stream, C.byref(n), C.byref(peak)), "a2t_resident")
+    return n.value, peak.value
 
 
 def a2t_read_layout(c: Cache, stream: int):

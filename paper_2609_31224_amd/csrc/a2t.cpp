@@ -1256,6 +1256,15 @@ int a2t_stream_info_get(const a2t_cache* c, int32_t stream, a2t_stream_info* out
     return A2T_OK;
 }
 
+int a2t_resident(const a2t_cache* c, int32_t stream, int32_t* n, int32_t* peak) {
+    if (!c || stream < 0 || stream >= c->cfg.n_streams) return A2T_ERR_INVALID;
+    if (c->dev_mode) return A2T_ERR_STATE;   // the device holds the state (a2t_dev_end)
+    const StreamState& s = c->ss[stream];
+    if (n) *n = s.resident();
+    if (peak) *peak = s.peak;
+    return A2T_OK;
+}
+
 int a2t_sync(a2t_cache* c) {
     if (!c) return A2T_ERR_INVALID;
     if (c->host_only) return A2T_OK;

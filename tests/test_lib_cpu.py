@@ -185,9 +185,12 @@ def _library_trace(spec, budget, window, unit_rows, kept_rows, max_step, rule=No
         moved0 = a2t.a2t_stream_info_get(c, 0)["moved_total"]
         n_ev, unmet = _evict(c, budget, window, rule)
         info = a2t.a2t_stream_info_get(c, 0)
+        assert a2t.a2t_resident(c, 0) == (info["resident"], info["peak"])
         rows.append((pre, int(n_ev[0]), bool(unmet[0]), info["resident"], info["last_evicted_unit"],
                      info["moved_total"] - moved0))
     peak = a2t.a2t_stream_info_get(c, 0)["peak"]
+    for bad in (-1, 1):
+        assert _status(a2t.a2t_resident, c, bad) == a2t.A2T_ERR_INVALID
     a2t.a2t_cache_destroy(c)
     return rows, peak
 
