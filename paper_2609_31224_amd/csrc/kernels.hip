@@ -13,7 +13,9 @@
 //               query row per stream).
 //   attn_valu   the same attention on the vector ALU, one query row per
 //               workgroup column: fp32 caches (chunk and decode).
-//   attn_merge  combines key-split partials (fixed order, deterministic).
+//   attn_merge  combines key-split partials (fixed order, deterministic): split
+//               groups combined in LDS, or one thread per row walking every
+//               split when a launch's streams have few splits.
 //   evict       eviction and compaction (Sec. 3.3): a ballot/prefix-sum scan
 //               over the passed-over ring rows keeps TEXT/RESPONSE/PREFIX rows
 //               and drops ACOUSTIC/DELIM rows of evicted units, moves the kept
@@ -1049,6 +1051,76 @@ __device__ __forceinline__ void merge_row_group(const DevState& st, const AttnDe
     for (int e2 = 0; e2 < EPT; ++e2) Elt<T>::store(op + e2, Ot[e2] * inv);
 }
 
+// Merge for launches whose streams have few key splits (fp16 partials of the
+// MFMA kernel): one thread per (query row, 8 output elements) walks every split
+// of its row itself, 8 at a time with all loads of a batch in flight, so a
+// workgroup covers 256 / (D / 8) rows (16 at head dim 128) and needs no LDS.
+// Splits combine in split order: deterministic.
+template <class BT>
+__global__ __launch_bounds__(256) void attn_merge_few_kernel(DevState st, BT b, bf16_t* o) {
+    constexpr int B = 8;
+    const AttnDesc d = b.d[blockIdx.z];
+    if (d.splits <= 1) return;
+    const int D = st.D, G = st.G, M = G * d.n_q;
+    const int tpr = D / 8, rows = 256 / tpr;
+    // row group rg of KV head g is linear block rg * Hkv + g, on the XCD of head g
+    const int g = blockIdx.x % st.Hkv, rg = blockIdx.x / st.Hkv;
+    const int rr = threadIdx.x / tpr, de = (threadIdx.x - rr * tpr) * 8;
+    const int mq = rg * rows + rr;
+    if (mq >= M) return;
+    const int ow = D / 2;   // floats per stored fp16 O row
+    const float* po = st.ws + d.ws_off;
+    const float* pml = po + (int64_t)d.splits * st.Hkv * M * ow;
+    const int64_t ostride = (int64_t)st.Hkv * M * ow, mstride = (int64_t)st.Hkv * M * 2;
+    const float* orow = po + ((int64_t)g * M + mq) * ow + de / 2;
+    const float* mrow = pml + ((int64_t)g * M + mq) * 2;
+    float mx = -INFINITY, L = 0.f, O[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) O[e] = 0.f;
+    for (int s0 = 0; s0 < d.splits; s0 += B) {
+        float2 ml[B];
+        u32x4 ov[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            const int s = s0 + j;
+            if (s < d.splits) {
+                ml[j] = *reinterpret_cast<const float2*>(mrow + s * mstride);
+                ov[j] = *reinterpret_cast<const u32x4*>(orow + s * ostride);
+            } else {
+                ml[j] = make_float2(-INFINITY, 0.f);
+                ov[j] = u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+        float bm = mx;
+#pragma unroll
+        for (int j = 0; j < B; ++j) bm = fmaxf(bm, ml[j].x);
+        if (bm == -INFINITY) continue;
+        const float c = (mx == -INFINITY) ? 0.f : exp2f(mx - bm);
+        L *= c;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) O[e] *= c;
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            // fp16 partials hold O / sum: weight exp2(m - bm) * sum
+            const float w0 = (ml[j].x == -INFINITY) ? 0.f : exp2f(ml[j].x - bm);
+            const float w = w0 * ml[j].y;
+            L += w;
+            const f16x8 h = __builtin_bit_cast(f16x8, ov[j]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) O[e] += w * (float)h[e];
+        }
+        mx = bm;
+    }
+    const float inv = 1.f / L;
+    const int i = mq / G, hh = mq - i * G;
+    uint16_t* op = reinterpret_cast<uint16_t*>(o) + ((int64_t)(d.q_row0 + i) * st.Hq + g * G + hh) * D + de;
+    *reinterpret_cast<uint2*>(op) = make_uint2(pack_bf16x2(O[0] * inv, O[1] * inv), pack_bf16x2(O[2] * inv, O[3] * inv));
+    *reinterpret_cast<uint2*>(op + 4) = make_uint2(pack_bf16x2(O[4] * inv, O[5] * inv), pack_bf16x2(O[6] * inv, O[7] * inv));
+}
+
+// launches whose streams have at most this many key splits merge with one thread
+// per row and element group (at most two load rounds of 8 per thread)
+constexpr int kMergeFewSplits = 16;
 // H16: the partials of the MFMA attention kernel (fp16 O rows); else fp32 (VALU kernel)
 template <typename T, int B, class BT, bool H16 = false>
 __global__ __launch_bounds__(256) void attn_merge_kernel(DevState st, BT b, T* o) {
@@ -1558,9 +1630,15 @@ hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o, hi
     const dim3 grid((G * b.max_rows + kMergeRows - 1) / kMergeRows * st.Hkv, 1, b.count);
     const int nsg = 256 / (kMergeRows * st.D / (h16 ? 8 : 4));    // split groups per workgroup
     const bool wide = (b.max_splits + nsg - 1) / nsg > 8;          // more than one round of 8
+    const bool few = h16 && b.max_splits <= kMergeFewSplits;
+    const int few_rows = 256 / (st.D / 8);
+    const dim3 few_grid((G * b.max_rows + few_rows - 1) / few_rows * st.Hkv, 1, b.count);
     return by_size<AttnBatchT>(b, [&](const auto& bb) {
         using B = std::decay_t<decltype(bb)>;
-        if (h16 && wide)
+        if (few)
+            A2T_DISPATCH((attn_merge_few_kernel<B>), few_grid, dim3(256), stream, kt, st, bb,
+                         static_cast<bf16_t*>(o));
+        else if (h16 && wide)
             A2T_DISPATCH((attn_merge_kernel<bf16_t, 12, B, true>), grid, dim3(256), stream, kt, st, bb,
                          static_cast<bf16_t*>(o));
         else if (h16)
