@@ -371,6 +371,7 @@ def timing_fields(step_ms, total_ms, steps, t_wall, t_enqueue):
 
 # ------------------------------------------------------------ ten-minute stream
 SESSION_UNITS = 600   # a ten-minute session of one-second units
+MAX_SESSIONS = 64     # sessions of one stream workload run (~0.9 GB of cache each)
 FILL_UNITS = 200      # the cache first exceeds the 4096-row budget near unit 186
 
 # The paper's own figures for this workload (context, not the target: whole-model
@@ -407,14 +408,21 @@ def run_stream(args):
     bring the cache to steady state untimed (eviction starts near unit 186), then
     --warmup more units run untimed and the next --steps units are timed; the
     session then runs on, untimed, to unit 600, whose peak residency gives the
-    peak-KV reduction.  Every timed unit lies inside the session."""
+    peak-KV reduction.  Every timed unit lies inside the session.  More --steps than
+    one session holds after the fill and the warm-up run over several sessions of
+    the same stream (independent streams of one cache, each brought to steady
+    state before the timed region): session s times units FILL_UNITS + --warmup
+    onward after session s - 1 has timed all of its own."""
     cfg = CONFIGS[1]
     first = FILL_UNITS + args.warmup
-    if args.warmup < 0 or args.steps < 1 or first + args.steps > SESSION_UNITS:
-        raise SystemExit(f"the timed units [{first}, {first + args.steps}) must lie inside the "
-                         f"{SESSION_UNITS}-unit session after the {FILL_UNITS}-unit fill: "
-                         f"--warmup + --steps <= {SESSION_UNITS - FILL_UNITS}")
-    last = first + args.steps
+    span = SESSION_UNITS - first             # timed units one session holds
+    if args.warmup < 0 or args.steps < 1 or span < 1:
+        raise SystemExit(f"--steps >= 1 and 0 <= --warmup < {SESSION_UNITS - FILL_UNITS}")
+    n_sess = -(-args.steps // span)
+    if n_sess > MAX_SESSIONS:
+        raise SystemExit(f"--steps {args.steps} needs {n_sess} sessions of {span} timed units; "
+                         f"at most {MAX_SESSIONS} fit (--steps <= {MAX_SESSIONS * span})")
+    last = first + min(args.steps, span)     # session 0's timed units are [first, last)
     spec = make_workload(cfg, seed=args.seed).streams[0]
     assert len(spec.steps) == SESSION_UNITS
     L, Hq, Hkv, D = cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
@@ -435,7 +443,7 @@ def run_stream(args):
         events (timing one layer in nine changes the unit time by ~3 %, all of them
         by ~40 %); "all": every dispatch of the timed units is timestamped (the
         per-kernel averages)."""
-        r = Runner(cfg, 1, unit_rows, keep_rows + 64, max_n)
+        r = Runner(cfg, n_sess, unit_rows, keep_rows + 64, max_n)
         torch, lib, h = r.torch, r.lib, r.h
         qp = torch.empty(POOL, L, max_n, Hq, D, dtype=torch.bfloat16, device=r.dev)
         kp = torch.empty(POOL, L, max_n, Hkv, D, dtype=torch.bfloat16, device=r.dev)
@@ -445,7 +453,7 @@ def run_stream(args):
             kp[p] = torch.from_numpy(vals["k"]).to(torch.bfloat16)
             vp[p] = torch.from_numpy(vals["v"]).to(torch.bfloat16)
         out = torch.empty(max_n, Hq, D, dtype=torch.bfloat16, device=r.dev)
-        ids = (C.c_int32 * 1)(0)
+        sess_ids = [(C.c_int32 * 1)(s) for s in range(n_sess)]
         budget = (C.c_int32 * 1)(cfg.budget)
         n_ev = (C.c_int32 * 1)()
         unmet = (C.c_uint8 * 1)()
@@ -455,7 +463,8 @@ def run_stream(args):
         o_ptr = out.data_ptr()
         R_log = []
 
-        def run_unit(u, record=False):
+        def run_unit(u, sess=0, record=False):
+            ids = sess_ids[sess]
             nrows, seg, pos, unit = metas[u]
             p = u % POOL
             for layer in range(L):
@@ -477,22 +486,28 @@ def run_stream(args):
                 if timed_layer:
                     r.a2t.a2t_profile_enable(r.cache, None)
             if record:
-                R_attn = r.stream_info(0).resident
+                info = r.stream_info(sess)
+                R_attn, moved0 = info.resident, info.moved_total
             r.check(lib.a2t_evict(h, 1, ids, budget, cfg.window, n_ev, unmet), "a2t_evict")
             if record:
-                R_log.append((R_attn, nrows[0], int(n_ev[0]), r.stream_info(0).moved_total))
+                R_log.append((R_attn, nrows[0], int(n_ev[0]),
+                              r.stream_info(sess).moved_total - moved0))
 
-        for u in range(first):
-            run_unit(u)
-        res = {"moved_before": r.stream_info(0).moved_total}
+        def timed_unit(j):
+            run_unit(first + j % span, j // span, record=True)
+
+        for sess in range(n_sess):
+            for u in range(first):
+                run_unit(u, sess)
+        res = {}
         if mode == "all":
-            res["kern"] = r.profiled(lambda j: run_unit(first + j, record=True), args.steps)
+            res["kern"] = r.profiled(timed_unit, args.steps)
         else:
             if mode == "attn":
                 r.a2t.a2t_profile_reserve(r.cache,
                                           args.steps * ((L + ATTN_SAMPLE - 1) // ATTN_SAMPLE))
             res["step_ms"], res["total_ms"], res["t_wall"], res["t_enq"] = r.timed(
-                lambda j: run_unit(first + j, record=True), args.steps)
+                timed_unit, args.steps)
         res["R_log"] = list(R_log)
         res["kern_timed"] = {}
         if mode == "attn":
@@ -516,21 +531,18 @@ def run_stream(args):
     total_ms = clean["total_ms"]
     ms_per_step = total_ms / args.steps
     # algorithmic bytes of the timed units
-    moved_prev, tot_bytes, moved_sum = clean["moved_before"], 0, 0
-    for (R_attn, n, _, moved_total) in R_log:
-        tot_bytes += step_bytes(R_attn, n, moved_total - moved_prev, R_attn, cfg)
-        moved_sum += moved_total - moved_prev
-        moved_prev = moved_total
+    tot_bytes, moved_sum = 0, 0
+    for (R_attn, n, _, moved) in R_log:
+        tot_bytes += step_bytes(R_attn, n, moved, R_attn, cfg)
+        moved_sum += moved
     step_gbps = tot_bytes / (total_ms * 1e-3) / 1e9
     if args.jsonl:
         # one record per timed unit: residency, rows appended / evicted / moved into the
         # kept region, algorithmic bytes and the unit's GPU time
         with open(args.jsonl, "w") as f:
-            moved_prev = clean["moved_before"]
-            for j, (R_attn, n, n_ev, moved_total) in enumerate(R_log):
-                moved = moved_total - moved_prev
-                moved_prev = moved_total
-                f.write(json.dumps({"unit": first + j, "resident_pre": R_attn, "appended": n,
+            for j, (R_attn, n, n_ev, moved) in enumerate(R_log):
+                f.write(json.dumps({"unit": first + j % span, "session": j // span,
+                                    "resident_pre": R_attn, "appended": n,
                                     "evicted": n_ev, "resident_post": R_attn - n_ev,
                                     "moved": moved,
                                     "alg_bytes": step_bytes(R_attn, n, moved, R_attn, cfg),
@@ -545,7 +557,8 @@ def run_stream(args):
     if not args.no_cpu_baseline:
         k = max(1, min(args.steps, args.cpu_sample_units))
         base_line = cpu_baseline(cfg, spec, args.seed, first, k, args.cpu_sample_layers)
-    traffic_units = [first, last]
+    # the committed counter summary covers one session's units [205, 225)
+    traffic_units = [first, last] if n_sess == 1 else [first, last, n_sess]
     res = {
         "value": 1000.0 / ms_per_step,
         "ms_per_step": ms_per_step,
@@ -556,12 +569,14 @@ def run_stream(args):
             "session_units": SESSION_UNITS,
             "fill_units": FILL_UNITS,
             "timed_units": [first, last],
+            "sessions": n_sess,
             "calls": "a2t_append + a2t_chunk_attn per layer" if args.unfused
                      else "a2t_append_attn per layer",
             "seed": args.seed,
         },
         "timed_window": {
             "units": [first, last],
+            "sessions": n_sess,
             "resident_rows_before_eviction": [int(min(resident)), int(max(resident))],
             "evicting_units": int(sum(1 for e in evicted if e > 0)),
             "rows_evicted": int(sum(evicted)),

@@ -21,6 +21,14 @@ def test_more_than_one_gpu_is_refused():
     assert "one GPU" in r.stderr and r.stdout == ""
 
 
+def test_stream_step_limits_are_checked_before_any_gpu_work():
+    # more steps than the sessions hold, and a warm-up past the session: clear errors
+    for flags, msg in ((["--steps", "100000"], "at most 64 fit"), (["--warmup", "400"], "--warmup <")):
+        r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *flags, "--no-cpu-baseline"],
+                           capture_output=True, text=True, timeout=120)
+        assert r.returncode != 0 and msg in r.stderr and r.stdout == ""
+
+
 def test_byte_formulas():
     cfg = CONFIGS[1]
     row = 2 * cfg.n_kv_heads * cfg.head_dim * 2            # K and V of one row, bf16: 4 KiB
