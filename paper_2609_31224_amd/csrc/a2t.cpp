@@ -323,7 +323,7 @@ void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_pe
         c->plan_force == c->force_splits && c->plan_limit == ws_limit) {
         int64_t ws = 0;
         for (int i = 0; i < n; ++i)
-            if (c->plan_splits[i] > 1) ws += c->plan_splits[i] * floats_per_split[i];
+            ws += stream_partials(c->plan_splits[i], floats_per_split[i]);
         if (ws <= ws_limit) {
             std::copy(c->plan_splits.begin(), c->plan_splits.begin() + n, splits);
             return;
@@ -342,7 +342,7 @@ void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_pe
             for (int i = 0; i < n; ++i) {
                 sp[i] = std::max(1, std::min((tiles[i] + budget - 1) / budget, kMaxSplits));
                 w += (int64_t)sp[i] * Hkv;
-                if (sp[i] > 1) ws += sp[i] * floats_per_split[i];
+                ws += stream_partials(sp[i], floats_per_split[i]);
             }
             if (ws > ws_limit) continue;
             const int64_t cost = launch_makespan(n, tiles, sp.data(), Hkv, c->target_wgs,
@@ -373,7 +373,7 @@ void plan_splits(a2t_cache* c, int n, const int* tiles, const int64_t* floats_pe
         int64_t ws = 0;
         int mx = 1;
         for (int i = 0; i < n; ++i) {
-            if (splits[i] > 1) ws += splits[i] * floats_per_split[i];
+            ws += stream_partials(splits[i], floats_per_split[i]);
             mx = std::max(mx, splits[i]);
         }
         if (ws <= ws_limit || mx == 1) break;
@@ -411,7 +411,7 @@ int64_t planned_partials(a2t_cache* c, int n, const int32_t* ids, const int32_t*
     plan_splits(c, n, tiles, floats, nsplit, ws_limit);
     int64_t total = 0;
     for (int i = 0; i < n; ++i)
-        if (nsplit[i] > 1) total += nsplit[i] * floats[i];
+        total += stream_partials(nsplit[i], floats[i]);
     return total;
 }
 
@@ -467,7 +467,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
         d.n_new = in_row0 ? s.step_rows : 0;
         d.in_row0 = in_row0 ? in_row0[i] : 0;
         d.ws_off = off;
-        if (d.splits > 1) off += (int64_t)d.splits * c->cfg.n_kv_heads * G * d.n_q * rf;
+        off += stream_partials(d.splits, (int64_t)c->cfg.n_kv_heads * G * d.n_q * rf);
     }
     // a fused step's own rows: when the launch's workgroups (with one more split
     // per tile holding them) still fit one round over the CUs, those tiles get
@@ -494,7 +494,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
                 }
             }
             wgs += (int64_t)ns[k] * Hkv;
-            if (ns[k] > 1) ws += (int64_t)ns[k] * Hkv * G * d.n_q * rf;
+            ws += stream_partials(ns[k], (int64_t)Hkv * G * d.n_q * rf);
         }
         if (any && wgs <= c->target_wgs && ws <= c->dev.ws_floats) {
             int64_t o2 = 0;
@@ -502,7 +502,7 @@ int attn_launch(a2t_cache* c, int layer, int n, const int32_t* ids, const int32_
                 AttnDesc& d = b.d[k];
                 d.splits = ns[k], d.tile_q = tq[k], d.tile_r = tr[k];
                 d.ws_off = o2;
-                if (d.splits > 1) o2 += (int64_t)d.splits * Hkv * G * d.n_q * rf;
+                o2 += stream_partials(d.splits, (int64_t)Hkv * G * d.n_q * rf);
                 splits = std::max(splits, (int)d.splits);
             }
             off = o2;

@@ -220,6 +220,12 @@ hipError_t launch_attn_merge(const DevState& st, const AttnBatch& b, void* o,
 // Floats of key-split partials per query row and head: O (fp16 from the MFMA kernel,
 // fp32 from the VALU kernel) and the fp32 (max, sum) pair.
 inline int64_t partial_row_floats(int head_dim, bool valu) { return (valu ? head_dim : head_dim / 2) + 2; }
+// Floats one stream's key-split partials take in the workspace (none without a
+// split), rounded up to 64 floats (256 bytes) so that every stream's rows start
+// 16-byte aligned for the kernels' 16-byte stores and loads.
+__host__ __device__ inline int64_t stream_partials(int splits, int64_t floats_per_split) {
+    return splits > 1 ? (splits * floats_per_split + 63) / 64 * 64 : 0;
+}
 hipError_t launch_evict(const DevState& st, const EvictBatch& b, hipStream_t stream,
                         const KTimer& kt);
 

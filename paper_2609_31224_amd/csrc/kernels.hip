@@ -1322,7 +1322,7 @@ __global__ __launch_bounds__(64) void dev_open_kernel(DevState st, DevStepArgs a
             const int t = max(1, (s_R[k] + kTileKeys - 1) / kTileKeys);
             const int sp = min((t + b - 1) / b, a.max_splits);
             wgs += (int64_t)sp * st.Hkv;
-            if (sp > 1) ws += (int64_t)sp * st.Hq * s_n[k] * row_floats;
+            ws += stream_partials(sp, (int64_t)st.Hq * s_n[k] * row_floats);
         }
         if (wgs <= a.target_wgs && ws <= st.ws_floats) {
             budget = b;
@@ -1342,11 +1342,11 @@ __global__ __launch_bounds__(64) void dev_open_kernel(DevState st, DevStepArgs a
         }
         const int t = max(1, (s_R[k] + kTileKeys - 1) / kTileKeys);
         int sp = min((t + budget - 1) / budget, a.max_splits);
-        if (sp > 1 && off + (int64_t)sp * st.Hq * s_n[k] * row_floats > st.ws_floats) sp = 1;
+        if (sp > 1 && off + stream_partials(sp, (int64_t)st.Hq * s_n[k] * row_floats) > st.ws_floats) sp = 1;
         d.splits = sp;
         d.tile_q = t / sp;
         d.tile_r = t % sp;
-        if (sp > 1) off += (int64_t)sp * st.Hq * s_n[k] * row_floats;
+        off += stream_partials(sp, (int64_t)st.Hq * s_n[k] * row_floats);
     }
 }
 

@@ -257,6 +257,31 @@ def test_device_planned_random_shapes(gpu, case):
           f"evictions {run.evictions} max err {run.max_err:.2e}", flush=True)
 
 
+def test_device_planned_odd_partial_blocks(gpu):
+    """Three query heads on three KV heads and three streams through the
+    device-planned calls: each stream's split partials start 16-byte aligned
+    whatever the odd row counts of the streams before it."""
+    import dataclasses
+    import paper_2609_31224_amd as a2t
+    cfg = dataclasses.replace(CONFIGS[0], index=310, n_q_heads=3, n_kv_heads=3, head_dim=64,
+                              dtype="bf16", n_streams=3, units=30, acoustic_rows=9,
+                              text_mean=2.0, text_cap=16, window=2)
+    specs = make_workload(cfg, seed=cfg.index).streams
+    budgets = [120, 200, 1000]
+    run = DevRun(cfg, cfg.index, specs, budgets, cfg.window, [0], 1, **_bounds(specs))
+    try:
+        a2t.a2t_dev_begin(run.cache)
+        for t in range(len(specs[0].steps)):
+            run.fill(t)
+            run.issue()
+            run.check(full=True)
+        a2t.a2t_dev_end(run.cache)
+    finally:
+        run.close()
+    print(f"[device odd partials] evictions {run.evictions} max err {run.max_err:.2e}", flush=True)
+    assert run.evictions > 0
+
+
 def test_device_planned_sink_rule_errors(gpu):
     """A budget below the sink count is refused on the device for that stream
     only (A2T_ERR_INVALID from a2t_dev_end, nothing evicted); the other stream

@@ -70,6 +70,21 @@ def test_random_shape_forced_valu(gpu, case):
         _env("A2T_FORCE_VALU", old)
 
 
+@pytest.mark.parametrize("case,dtype,fused", [(300, "bf16", True), (301, "bf16", False),
+                                             (302, "f32", False)])
+def test_odd_partial_blocks(gpu, case, dtype, fused):
+    """Three query heads on three KV heads (one query row per head and row), three
+    streams and three forced splits: a stream's split partials then take an odd
+    number of floats whenever its step has an odd row count, and the next stream's
+    partials must still start 16-byte aligned (MFMA kernel's fp16 partials, VALU
+    kernel's fp32 ones)."""
+    c = draw_case(case)
+    c["cfg"] = dataclasses.replace(c["cfg"], n_q_heads=3, n_kv_heads=3, dtype=dtype, n_streams=3,
+                                   varlen=True)
+    c.update(fused=fused, splits="3", rule=None)
+    _run_case(c, f"odd partials {case} {dtype}")
+
+
 def _run_case(c, label):
     cfg = c["cfg"]
     specs = make_workload(cfg, seed=cfg.index).streams
