@@ -30,7 +30,10 @@
  *   - "device" pointers are HIP device memory (e.g. torch CUDA tensors on
  *     ROCm); "host" pointers are ordinary CPU memory, read before the call
  *     returns.  Device buffers must stay valid until the HIP stream reaches
- *     the enqueued work; outputs are ready after the stream does.
+ *     the enqueued work; outputs are ready after the stream does.  The K, V,
+ *     Q and O buffers of the append and attention calls must be 16-byte
+ *     aligned (the kernels move them 16 bytes at a time): A2T_ERR_INVALID
+ *     otherwise.
  *   - All compute is enqueued on the cache's HIP stream (a2t_set_stream).
  *     Nothing in a2t_append / a2t_append_attn / a2t_chunk_attn /
  *     a2t_decode_attn / a2t_evict / a2t_evict_rule allocates memory (every

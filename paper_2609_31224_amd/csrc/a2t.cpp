@@ -415,6 +415,9 @@ int64_t planned_partials(a2t_cache* c, int n, const int32_t* ids, const int32_t*
     return total;
 }
 
+// the kernels move K, V, Q and O rows 16 bytes at a time
+static bool unaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
 // One attention launch (plus merge) over up to kMaxDesc streams.
 // With in_row0 non-null (bf16 MFMA path only) the launch also appends each
 // stream's open-step rows of `layer` from k_in / v_in.
@@ -545,7 +548,7 @@ int attn_common(a2t_cache* c, int32_t layer, int32_t n_streams, const int32_t* i
     if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
     int rc = check_streams(c, n_streams, ids);
     if (rc) return rc;
-    if (!q || !o || (!decode && !n_q)) return A2T_ERR_INVALID;
+    if (!q || !o || unaligned16(q) || unaligned16(o) || (!decode && !n_q)) return A2T_ERR_INVALID;
     std::vector<int32_t>& nq = c->tmp_nq;
     std::vector<int32_t>& row0 = c->tmp_row0;
     int32_t acc = 0;
@@ -791,7 +794,7 @@ static int append_impl(a2t_cache* c, int32_t layer, int32_t n_streams, const int
     int rc = check_streams(c, n_streams, ids);
     if (rc) return rc;
     if (!n_rows) return A2T_ERR_INVALID;
-    if (!c->host_only && (!kin || !vin)) return A2T_ERR_INVALID;
+    if (!c->host_only && (!kin || !vin || unaligned16(kin) || unaligned16(vin))) return A2T_ERR_INVALID;
     const bool opens = (layer == 0 || layer == A2T_ALL_LAYERS);
     if (opens && (!seg || !pos || !unit_id)) return A2T_ERR_INVALID;
 
@@ -989,7 +992,8 @@ int append_attn_args(a2t_cache* c, int32_t layer, int32_t n_streams, const int32
     if (c->poisoned) return A2T_ERR_HIP;
     if (c->dev_mode) return A2T_ERR_STATE;
     if (layer < 0 || layer >= c->cfg.n_layers) return A2T_ERR_INVALID;
-    if (!n_rows || !n_q || !q || !o || n_streams < 1 || n_streams > c->cfg.n_streams)
+    if (!n_rows || !n_q || !q || !o || unaligned16(q) || unaligned16(o) || n_streams < 1 ||
+        n_streams > c->cfg.n_streams)
         return A2T_ERR_INVALID;
     for (int i = 0; i < n_streams; ++i)
         if (n_q[i] < 1 || n_q[i] > n_rows[i]) return A2T_ERR_INVALID;
@@ -1519,6 +1523,7 @@ int a2t_dev_append_attn(a2t_cache* c, int32_t layer, const void* k, const void* 
     if (c->poisoned) return A2T_ERR_HIP;
     if (!c->dev_mode || !c->dev_step_open) return A2T_ERR_STATE;
     if (layer < 0 || layer >= c->cfg.n_layers || !k || !v || !q || !o) return A2T_ERR_INVALID;
+    if (unaligned16(k) || unaligned16(v) || unaligned16(q) || unaligned16(o)) return A2T_ERR_INVALID;
     if (c->dev_layers[layer]) return A2T_ERR_STATE;
     DeviceGuard dg(c->cfg.device);
     if (launch_attn_tile_dev(c->dev, c->dplan, c->dev_count, c->dev_max_splits, layer, q, o, k, v,

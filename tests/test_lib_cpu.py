@@ -128,6 +128,9 @@ def test_append_errors_leave_state_unchanged():
     # attention on a host-only cache is refused
     assert _status(a2t.a2t_chunk_attn, c, 0, [0], [1], 16, 32) == a2t.A2T_ERR_NODEV
     assert _status(a2t.a2t_chunk_attn, c, 0, [0], [1], 0, 32) == a2t.A2T_ERR_INVALID
+    # device buffers must be 16-byte aligned
+    assert _status(a2t.a2t_chunk_attn, c, 0, [0], [1], 24, 32) == a2t.A2T_ERR_INVALID
+    assert _status(a2t.a2t_chunk_attn, c, 0, [0], [1], 16, 40) == a2t.A2T_ERR_INVALID
     assert _status(a2t.a2t_chunk_attn, c, 0, [0], [4], 16, 32) == a2t.A2T_ERR_STATE  # > step rows
     a2t.a2t_cache_destroy(c)
 
