@@ -358,6 +358,8 @@ def roofline(kernel, kern, alg_bytes, workload, units=None):
             "launches_timed": kern.get(kernel, {}).get("launches"),
             "alg_bytes_per_launch": alg_bytes,
             "traffic_over_alg": traffic / alg_bytes if traffic else None,
+            # the counters' HBM bytes over the same mean dispatch duration
+            "traffic_gbps": traffic / (us * 1e-6) / 1e9 if traffic and us else None,
             "timing": "per-dispatch start/stop events on the cache's stream, in a second pass "
                       "over the timed steps"}
 

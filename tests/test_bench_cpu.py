@@ -54,6 +54,17 @@ def test_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
     assert bench.measured_traffic("stream", "attn_tile", [205, 225]) is None
 
 
+def test_roofline_fields():
+    kern = {"attn_tile": {"launches": 80, "avg_us": 10.0}}
+    r = bench.roofline("attn_tile", kern, 17.2e6, "stream", [205, 225])
+    assert abs(r["achieved"] - 1720.0) < 1e-9 and abs(r["frac"] - 0.215) < 1e-12
+    assert r["traffic"] is not None and abs(r["traffic_gbps"] - r["traffic"] / 10e-6 / 1e9) < 1e-9
+    assert abs(r["traffic_over_alg"] - r["traffic"] / 17.2e6) < 1e-12
+    r = bench.roofline("attn_tile", kern, 17.2e6, "stream", [5, 25])   # other units: no counters
+    assert r["traffic"] is None and r["traffic_gbps"] is None and r["traffic_over_alg"] is None
+    assert bench.roofline("attn_tile", {}, 17.2e6, "stream")["achieved"] is None
+
+
 def _check_baseline(b, unit):
     assert b["kind"] == "oracle" and b["unit"] == unit
     assert b["value"] > 0 and b["cores"] >= 1 and b["sample"]
