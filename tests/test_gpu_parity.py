@@ -197,6 +197,24 @@ def test_edge_streams(gpu, dtype, tol, budget, window):
 
 
 @pytest.mark.parametrize("fused", [False, True])
+def test_maximum_step_rows(gpu, fused):
+    """A step of the library's maximum size (max_step_rows = 1024): a 1024-row
+    prefix at the config-1 head shape (32/8 heads, head dim 128, bf16) gives 4,096
+    query rows per KV head, 32 passes of the MFMA kernel over its keys; then units
+    that evict down to the budget around the prefix, which is never evicted."""
+    cfg = CONFIGS[1]
+    spec = tiny_stream([[1] * 17 + [2, 3, 3, 3, 2]] * 8, prefix=1024)
+    ls = Lockstep(cfg, 13, [spec], layers_checked=[0], n_layers=1, budgets=[1100], window=1,
+                  tol=BF16_TOL, unit_rows=1024 + 400, kept_rows=1100, max_step=1024, fused=fused)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    _report(ls, f"max step rows fused={fused}")
+    assert ls.evictions > 0
+
+
+@pytest.mark.parametrize("fused", [False, True])
 def test_edge_streams_config1_heads(gpu, fused):
     """The edge units at the config-1 head shape (32/8 heads, head dim 128, bf16):
     the 84-row unit (64 transcript tokens) gives 336 query rows per KV head, three
